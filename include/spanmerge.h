@@ -1,0 +1,289 @@
+/*
+ * spanmerge.h -- C ABI of the span-merging (UMIM) inference hot path on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The method ("Distilling Sequential Computation in Transformer Language
+ * Models", arXiv 2609.27233) replaces a span of n input tokens by one
+ * surrogate embedding produced by a small attention-pooling merge module
+ * M_phi (Sec. 3.2 Eq. 1; appendix "Module Architecture and Integration").
+ * At inference it compresses prompts before prefill and, during decoding,
+ * rolls back the n-1 cached entries of a freshly completed span and appends
+ * the surrogate's single K/V state (appendix "Inference with UMIM: Prompt and
+ * Decoding-Time Merging").  Every later decode step then attends over the
+ * shorter cache.  The five calls below are the device-side steps of that
+ * path:
+ *
+ *   sm_merge_spans      z_s = M_phi(e(x_span))            for every span s
+ *   sm_pack_spans       keep mask -> compressed positions -> packed rows
+ *   sm_kv_rollback      crop k entries from the tail of each listed sequence
+ *   sm_kv_append        append K/V rows (one surrogate state, or a prompt)
+ *   sm_decode_attention one query per sequence over its whole paged cache
+ *
+ * General rules for every call
+ * ----------------------------
+ *  - Every pointer is a DEVICE pointer unless its comment says (host).
+ *  - The caller owns every buffer (tables, pools, workspaces, outputs); the
+ *    library allocates nothing, keeps no global state and never synchronizes.
+ *    Work is enqueued on `stream` (0 = the null stream); pointers must stay
+ *    valid until that work has completed.  Calls are safe to capture in a
+ *    HIP graph.
+ *  - Synchronous status: SM_EINVAL for arguments the host can check (null
+ *    pointers, unsupported shapes, a workspace that is too small); SM_EHIP if
+ *    a kernel launch fails.  Nothing is enqueued when a call returns non-OK.
+ *  - Asynchronous status: problems only visible to the device (indices read
+ *    from device memory) OR a bit into a device error word `err`
+ *    (SM_ERR_EINVAL / SM_ERR_ERANGE / SM_ERR_ENOMEM).  The word is sticky: a
+ *    mutating cache call (rollback, append) that finds `*err != 0` when it
+ *    starts does nothing, so a failed call leaves the cache exactly as it
+ *    was (all-or-nothing) and the cache stays frozen until the caller has
+ *    read and cleared the word.  Exactly one bit is set per failing call,
+ *    checked in the order EINVAL, ERANGE, ENOMEM.  No index read from device
+ *    memory is ever used to address memory before it has been range-checked.
+ *
+ * Dtypes: SM_F32 (fp32 storage, fp32 arithmetic) and SM_BF16 (bf16 storage,
+ * fp32 accumulation, outputs rounded to nearest-even bf16).
+ */
+#ifndef SPANMERGE_H
+#define SPANMERGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { SM_F32 = 0, SM_BF16 = 1 } sm_dtype;
+
+typedef enum {
+  SM_OK = 0,
+  SM_EINVAL = 1, /* bad argument */
+  SM_ERANGE = 2, /* length / capacity out of range */
+  SM_ENOMEM = 3, /* not enough free KV blocks */
+  SM_EHIP = 4    /* a HIP launch failed */
+} sm_status;
+
+/* bits of the device error word */
+enum { SM_ERR_EINVAL = 1, SM_ERR_ERANGE = 2, SM_ERR_ENOMEM = 4 };
+
+/* Largest number of requests (sequences) in one rollback / append call. */
+#define SM_MAX_REQUESTS 1024
+
+/*
+ * Parameters phi of the merge module M_phi (appendix "Attention-based Pooling
+ * Architecture" and "Parameter Count": |phi| = 2d^2 + 7d).  Storage dtype is
+ * the call's dtype.  Linear layers compute y = W x + b with W stored
+ * row-major [out = d][in = d].  The pooling splits the d features into h
+ * contiguous head blocks of d_h = d / h features.
+ */
+typedef struct {
+  int d;            /* model width (= M_phi width) */
+  int h;            /* pooling heads; the paper uses 4 */
+  float ln_eps;     /* LayerNorm epsilon (1e-5) */
+  const void *Q;    /* [h][d_h] learned pooling queries q_i */
+  const void *W_kv; /* [d][d] token projection Linear_kv */
+  const void *b_kv; /* [d] */
+  const void *g_kv; /* [d] LN_kv gain */
+  const void *beta_kv; /* [d] LN_kv bias */
+  const void *W_o;  /* [d][d] output projection Linear_o */
+  const void *b_o;  /* [d] */
+  const void *g_o;  /* [d] LN_o gain */
+  const void *beta_o;  /* [d] LN_o bias */
+} sm_merge_params;
+
+/*
+ * Paged KV cache of one attention layer, over caller-owned buffers.
+ *
+ *  k_pool  [num_blocks][num_kv_heads][block_size][head_dim]  token-major pages
+ *  v_pool  [num_blocks][num_kv_heads][head_dim][block_size]  dim-major pages
+ *          (V is stored transposed inside each page so that the decode
+ *          kernel can feed it to the matrix cores without a transpose)
+ *  block_table [max_seqs][max_blocks_per_seq]  physical block of each logical
+ *          block, -1 when unmapped
+ *  lengths     [max_seqs]   cached entries per sequence
+ *  free_stack  [num_blocks] LIFO stack of free physical blocks; the next pop
+ *          returns free_stack[*free_top - 1]
+ *  free_top    [1]
+ *  err         [1]          sticky device error word (see above)
+ *
+ * Entry j of sequence s lives in block block_table[s][j / block_size] at
+ * slot j % block_size.  head_dim must be 64 or 128; block_size must be a
+ * power of two in [16, 512].
+ */
+typedef struct {
+  sm_dtype dtype;
+  int num_kv_heads;
+  int head_dim;
+  int block_size;
+  int num_blocks;
+  int max_seqs;
+  int max_blocks_per_seq;
+  void *k_pool;
+  void *v_pool;
+  int32_t *block_table;
+  int32_t *lengths;
+  int32_t *free_stack;
+  int32_t *free_top;
+  int32_t *err;
+} sm_paged_cache;
+
+/* Human-readable name of a status code (host, static storage). */
+const char *sm_status_string(sm_status s);
+
+/* Bytes of workspace sm_merge_spans needs for these sizes. */
+size_t sm_merge_workspace_bytes(int total_rows, int num_spans, int d,
+                                sm_dtype dt);
+
+/*
+ * sm_merge_spans -- z_s = M_phi(E_s) for every span s in one launch sequence
+ * (Sec. 3.2 Eq. 1; the appendix form with GELU and LayerNorm in
+ * "Attention-based Pooling Architecture"):
+ *
+ *   P   = LN_kv(GELU(Linear_kv(E_s)))                 E_s: the span's n rows
+ *   a_i = softmax_j(P[j, head i] . q_i / sqrt(d_h)),  o_i = sum_j a_i[j] P[j, head i]
+ *   z_s = LN_o(GELU(Linear_o([o_1; ...; o_h])))
+ *
+ * GELU is the exact erf form; LayerNorm uses the biased variance.
+ *
+ *  emb           [emb_rows][d] static embedding table (dtype dt)
+ *  row_idx       [total_rows] row of emb for each span token, spans stored
+ *                back to back (CSR)
+ *  span_offsets  [num_spans + 1] span s owns row_idx[span_offsets[s] ..
+ *                span_offsets[s+1]); span_offsets[0] = 0,
+ *                span_offsets[num_spans] = total_rows, every span has n >= 1
+ *  total_rows    (host) sum of span lengths
+ *  p             (host) parameters; d % h == 0, d % 256 == 0, d / h % 64 == 0
+ *  out           [num_spans][d] surrogates (dtype dt)
+ *  ws, ws_bytes  workspace of at least sm_merge_workspace_bytes(...) bytes
+ *  err           [1] device error word: EINVAL when a row index is outside
+ *                [0, emb_rows) or the span offsets are not a valid CSR
+ *                (the affected surrogates are then zero)
+ */
+sm_status sm_merge_spans(const void *emb, int64_t emb_rows,
+                         const int32_t *row_idx, int total_rows,
+                         const int32_t *span_offsets, int num_spans,
+                         const sm_merge_params *p, sm_dtype dt, void *out,
+                         void *ws, size_t ws_bytes, int32_t *err,
+                         hipStream_t stream);
+
+/*
+ * sm_pack_spans -- prompt compression bookkeeping (appendix "Prompt-time
+ * Integration"; "Inference with UMIM", paragraph "Prompt Merging").
+ * A merged span keeps only its LAST position (its surrogate is anchored
+ * there: "Mask Construction and Sequence Alignment"); compressed positions
+ * are contiguous ("Positional Encoding under Token-Span Merging":
+ * pi(t) = t - r(t)).  For sequence b with tokens [seq_offsets[b],
+ * seq_offsets[b+1]):
+ *
+ *   keep[t]   = 0 if t lies in a span and is not its last token, else 1
+ *   pi[t]     = sum_{t' < t, same sequence} keep[t']   (span tokens all get
+ *               their surrogate's position)
+ *   L~_b      = (#tokens of b) - sum_{spans of b} (n - 1)
+ *   packed_offsets[b] = sum_{b' < b} L~_b'
+ *   packed_src[packed_offsets[b] + pi[t]] = t (global token index) for a
+ *               token outside every span, and -1 - s for span s
+ *   packed[...] (optional) = emb[token_ids[t]] or surrogates[s], same rule
+ *
+ *  seq_offsets      [B + 1] token ranges of the B sequences
+ *  total_tokens     (host) seq_offsets[B]
+ *  span_start       [num_spans] global token index where span s starts
+ *  span_len         [num_spans] n >= 1
+ *  seq_span_offsets [B + 1] spans of sequence b are [seq_span_offsets[b],
+ *                   seq_span_offsets[b+1]), sorted by start, non-overlapping
+ *  pi               [total_tokens] out
+ *  packed_offsets   [B + 1] out
+ *  packed_src       [total_tokens] out (capacity; sum L~ entries written)
+ *  token_ids, emb, surrogates, packed: only used when packed != NULL;
+ *                   packed is [total_tokens][d] capacity, dtype dt
+ *  err              [1] EINVAL when the span list is not sorted,
+ *                   non-overlapping and inside its sequence, or a token id
+ *                   is outside [0, emb_rows)
+ */
+sm_status sm_pack_spans(int B, const int32_t *seq_offsets, int total_tokens,
+                        int num_spans, const int32_t *span_start,
+                        const int32_t *span_len,
+                        const int32_t *seq_span_offsets, int32_t *pi,
+                        int32_t *packed_offsets, int32_t *packed_src,
+                        const int32_t *token_ids, const void *emb,
+                        int64_t emb_rows, const void *surrogates, int d,
+                        sm_dtype dt, void *packed, int32_t *err,
+                        hipStream_t stream);
+
+/*
+ * sm_kv_rollback -- the decoding-time cache crop (appendix "Decoding-time
+ * Integration" and "Decoding-Time Merging and KV-Cache Update": crop the n-1
+ * cached entries of a matched span, L_C' = L_C - (n-1) + 1 once the
+ * surrogate is appended).  For request i: lengths[seq_ids[i]] -= k[i].
+ * Logical blocks no longer needed are unmapped (-1) and pushed on the free
+ * stack; requests are processed in reverse list order, and within a request
+ * from the highest logical block down.  KV bytes are not touched.
+ *
+ *  c        (host) cache descriptor
+ *  seq_ids  [n] distinct sequence ids in [0, max_seqs)
+ *  k        [n] 0 <= k[i] <= lengths[seq_ids[i]]
+ *  n        (host) 0 <= n <= min(max_seqs, SM_MAX_REQUESTS)
+ * Device errors: EINVAL (id out of range, duplicate id, k < 0),
+ * ERANGE (k > length).
+ */
+sm_status sm_kv_rollback(const sm_paged_cache *c, const int32_t *seq_ids,
+                         const int32_t *k, int n, hipStream_t stream);
+
+/*
+ * sm_kv_append -- append K/V rows at the tail of each listed sequence; the
+ * surrogate's single-step state after a rollback (Decoding-Time Merging: the
+ * surrogate forward "produces one new key and value state"), one ordinary
+ * token per decode step, or a whole compressed prompt.  Requests are served
+ * in list order; for each row the slot is pos = lengths[s], a block is
+ * popped from the free stack when pos % block_size == 0, then the row is
+ * copied and lengths[s] += 1.
+ *
+ *  seq_ids      [n] distinct sequence ids
+ *  row_offsets  [n + 1] request i appends rows [row_offsets[i],
+ *               row_offsets[i+1]) of K and V; row_offsets[0] = 0,
+ *               row_offsets[n] = total_rows
+ *  total_rows   (host)
+ *  K, V         [total_rows][num_kv_heads][head_dim] (cache dtype)
+ * Device errors: EINVAL (bad id, duplicate, bad offsets), ERANGE
+ * (length would exceed max_blocks_per_seq * block_size), ENOMEM (not enough
+ * free blocks for the whole call).
+ */
+sm_status sm_kv_append(const sm_paged_cache *c, const int32_t *seq_ids,
+                       const int32_t *row_offsets, int n, int total_rows,
+                       const void *K, const void *V, hipStream_t stream);
+
+/* Bytes of workspace sm_decode_attention needs for these sizes. */
+size_t sm_decode_workspace_bytes(int n, int num_q_heads, int head_dim,
+                                 int max_len);
+
+/*
+ * sm_decode_attention -- one decode query per sequence attending over all
+ * lengths[s] cached entries (the unchanged backbone attention the paper's
+ * throughput study measures, "Efficiency Analysis"):
+ *
+ *   out[i, h] = sum_j softmax_j(scale * q[i, h] . K[s, j, g]) V[s, j, g]
+ *   s = seq_ids[i],  g = h / (num_q_heads / num_kv_heads)   (grouped query)
+ *
+ * A sequence of length 0 gives zeros.  Implemented as split-K (partials
+ * over chunks of the cache) followed by an exact combine.
+ *
+ *  seq_ids      [n] ids in [0, max_seqs) (repeats allowed)
+ *  q            [n][num_q_heads][head_dim] (cache dtype)
+ *  num_q_heads  (host) multiple of num_kv_heads, group size <= 16
+ *  max_len      (host) upper bound on lengths[seq_ids[i]]; sizes the grid
+ *  out          [n][num_q_heads][head_dim] (cache dtype)
+ *  ws, ws_bytes at least sm_decode_workspace_bytes(n, num_q_heads,
+ *               head_dim, max_len)
+ * Device errors (into c->err; the affected rows are zero): EINVAL (bad id,
+ * block id out of range), ERANGE (length > max_len).
+ */
+sm_status sm_decode_attention(const sm_paged_cache *c, const int32_t *seq_ids,
+                              int n, const void *q, int num_q_heads,
+                              float scale, int max_len, void *out, void *ws,
+                              size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPANMERGE_H */

@@ -1,0 +1,261 @@
+"""CPU oracle of the span-merging inference hot path (test infrastructure).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s CPU-baseline
+leg may import this package.  It wraps ``liboracle.so`` (plain C, double
+precision, OpenMP) with ctypes and numpy; it never imports the GPU package
+and the GPU package never imports it.  Inputs reach both sides only through
+the seeded generators.
+
+Floating inputs are passed as float64 (bf16 and fp32 values widen exactly);
+cache pools hold raw storage elements (uint16 bf16 bit patterns or float32)
+so that copies compare bit for bit.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+OK, EINVAL, ERANGE, ENOMEM = 0, 1, 2, 3
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so next to its source (gcc, -O2, OpenMP)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+               "-Wall", "-Wextra", "-Wno-unused-parameter",
+               _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        _lib = C.CDLL(_LIB_PATH)
+        _declare(_lib)
+    return _lib
+
+
+_P = C.c_void_p
+_I = C.c_int
+_L = C.c_int64
+_D = C.c_double
+
+
+class _Cache(C.Structure):
+    _fields_ = [("is_bf16", _I), ("num_kv_heads", _I), ("head_dim", _I),
+                ("block_size", _I), ("num_blocks", _I), ("max_seqs", _I),
+                ("max_blocks_per_seq", _I), ("k_pool", _P), ("v_pool", _P),
+                ("block_table", _P), ("lengths", _P), ("free_stack", _P),
+                ("free_top", _P)]
+
+
+def _declare(L):
+    L.orc_merge_spans.argtypes = [_I, _I, _D, _P, _L, _P, _P, _I, _P, _P, _P,
+                                  _P, _P, _P, _P, _P, _P, _I, _P, _P, _I]
+    L.orc_merge_spans.restype = _I
+    L.orc_pack_spans.argtypes = [_I, _P, _I, _P, _P, _P, _P, _P, _P, _P, _P,
+                                 _L, _P, _I, _I, _P]
+    L.orc_pack_spans.restype = _I
+    L.orc_kv_rollback.argtypes = [C.POINTER(_Cache), _P, _P, _I]
+    L.orc_kv_rollback.restype = _I
+    L.orc_kv_append.argtypes = [C.POINTER(_Cache), _P, _P, _I, _P, _P]
+    L.orc_kv_append.restype = _I
+    L.orc_decode_attention.argtypes = [C.POINTER(_Cache), _P, _I, _P, _I, _D,
+                                       _P, _P, _I]
+    L.orc_decode_attention.restype = _I
+    L.orc_layer_qkv.argtypes = [_I, _I, _P, _P, _I, _I, _I, _D, _D, _P, _P,
+                                _P, _P, _P, _P]
+    L.orc_layer_qkv.restype = None
+    L.orc_num_threads.argtypes = []
+    L.orc_num_threads.restype = _I
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def num_threads() -> int:
+    return lib().orc_num_threads()
+
+
+# --------------------------------------------------------------------------
+# merge module
+
+PARAM_NAMES = ("Q", "W_kv", "b_kv", "g_kv", "beta_kv", "W_o", "b_o", "g_o",
+               "beta_o")
+
+
+def merge_spans(emb, row_idx, span_offsets, params, h, ln_eps=1e-5, flags=0,
+                return_weights=False):
+    """M_phi for every span; returns float64 [S, d] (and pooling weights
+    [S, h, max_n] when asked).  ``params`` maps PARAM_NAMES to arrays."""
+    emb = _f64(emb)
+    d = emb.shape[1]
+    row_idx = _i32(row_idx)
+    span_offsets = _i32(span_offsets)
+    S = span_offsets.shape[0] - 1
+    p = {k: _f64(params[k]) for k in PARAM_NAMES}
+    out = np.zeros((max(S, 0), d), dtype=np.float64)
+    n_max = int(np.max(np.diff(span_offsets))) if S > 0 else 1
+    w = np.zeros((max(S, 0), h, n_max)) if return_weights else None
+    st = lib().orc_merge_spans(
+        d, h, ln_eps, _ptr(emb), emb.shape[0], _ptr(row_idx),
+        _ptr(span_offsets), S, *(_ptr(p[k]) for k in PARAM_NAMES), flags,
+        _ptr(out), _ptr(w), n_max)
+    if return_weights:
+        return st, out, w
+    return st, out
+
+
+# --------------------------------------------------------------------------
+# prompt packing
+
+def pack_spans(seq_offsets, span_start, span_len, seq_span_offsets,
+               token_ids=None, emb_raw=None, surrogates_raw=None):
+    """Returns (status, dict(pi, packed_offsets, packed_src, packed)).
+    ``emb_raw`` / ``surrogates_raw`` are raw-storage arrays (uint16 for bf16,
+    float32 for fp32) of shape [rows, d]; packed rows are byte copies."""
+    seq_offsets = _i32(seq_offsets)
+    B = seq_offsets.shape[0] - 1
+    total = int(seq_offsets[-1])
+    span_start, span_len = _i32(span_start), _i32(span_len)
+    seq_span_offsets = _i32(seq_span_offsets)
+    S = span_start.shape[0]
+    pi = np.full(total, -7, dtype=np.int32)
+    packed_offsets = np.full(B + 1, -7, dtype=np.int32)
+    packed_src = np.full(total, -7, dtype=np.int32)
+    packed = None
+    d, eb, emb_rows = 0, 0, 0
+    if emb_raw is not None:
+        emb_raw = np.ascontiguousarray(emb_raw)
+        surrogates_raw = np.ascontiguousarray(surrogates_raw)
+        token_ids = _i32(token_ids)
+        d = emb_raw.shape[1]
+        eb = emb_raw.dtype.itemsize
+        emb_rows = emb_raw.shape[0]
+        packed = np.zeros((total, d), dtype=emb_raw.dtype)
+    st = lib().orc_pack_spans(
+        B, _ptr(seq_offsets), S, _ptr(span_start), _ptr(span_len),
+        _ptr(seq_span_offsets), _ptr(pi), _ptr(packed_offsets),
+        _ptr(packed_src), _ptr(token_ids), _ptr(emb_raw), emb_rows,
+        _ptr(surrogates_raw), d, eb, _ptr(packed))
+    res = dict(pi=pi, packed_offsets=packed_offsets, packed_src=packed_src)
+    if st == OK:
+        n = int(packed_offsets[-1])
+        res["packed_src"] = packed_src[:n].copy()
+        if packed is not None:
+            res["packed"] = packed[:n].copy()
+    return st, res
+
+
+# --------------------------------------------------------------------------
+# paged KV cache
+
+class OracleCache:
+    """Paged cache held in numpy arrays, driven by the C oracle."""
+
+    def __init__(self, *, bf16, num_kv_heads, head_dim, block_size,
+                 num_blocks, max_seqs, max_blocks_per_seq, free_order=None):
+        self.is_bf16 = bool(bf16)
+        self.H, self.D, self.bs = num_kv_heads, head_dim, block_size
+        self.num_blocks, self.max_seqs = num_blocks, max_seqs
+        self.max_blocks = max_blocks_per_seq
+        dt = np.uint16 if bf16 else np.float32
+        self.k_pool = np.zeros((num_blocks, num_kv_heads, block_size, head_dim), dtype=dt)
+        self.v_pool = np.zeros((num_blocks, num_kv_heads, head_dim, block_size), dtype=dt)
+        self.block_table = np.full((max_seqs, max_blocks_per_seq), -1, dtype=np.int32)
+        self.lengths = np.zeros(max_seqs, dtype=np.int32)
+        # the stack pops from the top: free_stack[top-1] is handed out first
+        order = np.arange(num_blocks, dtype=np.int32) if free_order is None else _i32(free_order)
+        self.free_stack = order[::-1].copy()
+        self.free_top = np.array([num_blocks], dtype=np.int32)
+
+    def _struct(self):
+        return _Cache(int(self.is_bf16), self.H, self.D, self.bs,
+                      self.num_blocks, self.max_seqs, self.max_blocks,
+                      _ptr(self.k_pool), _ptr(self.v_pool),
+                      _ptr(self.block_table), _ptr(self.lengths),
+                      _ptr(self.free_stack), _ptr(self.free_top))
+
+    def rollback(self, seq_ids, k):
+        seq_ids, k = _i32(seq_ids), _i32(k)
+        s = self._struct()
+        return lib().orc_kv_rollback(C.byref(s), _ptr(seq_ids), _ptr(k), seq_ids.shape[0])
+
+    def append(self, seq_ids, row_offsets, K, V):
+        """K, V: raw-storage arrays [rows, H, D] (uint16 bf16 bits or float32)."""
+        seq_ids, row_offsets = _i32(seq_ids), _i32(row_offsets)
+        dt = np.uint16 if self.is_bf16 else np.float32
+        K = np.ascontiguousarray(K, dtype=dt)
+        V = np.ascontiguousarray(V, dtype=dt)
+        s = self._struct()
+        return lib().orc_kv_append(C.byref(s), _ptr(seq_ids), _ptr(row_offsets),
+                                   seq_ids.shape[0], _ptr(K), _ptr(V))
+
+    def decode_attention(self, seq_ids, q, num_q_heads, scale, return_probs=False):
+        seq_ids = _i32(seq_ids)
+        q = _f64(q)
+        n = seq_ids.shape[0]
+        out = np.zeros((n, num_q_heads, self.D))
+        probs = None
+        stride = 1
+        if return_probs:
+            stride = max(1, int(self.lengths[seq_ids].max()) if n else 1)
+            probs = np.zeros((n, num_q_heads, stride))
+        s = self._struct()
+        st = lib().orc_decode_attention(C.byref(s), _ptr(seq_ids), n, _ptr(q),
+                                        num_q_heads, scale, _ptr(out), _ptr(probs), stride)
+        if return_probs:
+            return st, out, probs
+        return st, out
+
+    # logical view helpers (pure indexing, used by tests)
+    def logical_kv(self, s):
+        """Raw K [L, H, D] and V [L, H, D] of sequence s in cache order."""
+        L = int(self.lengths[s])
+        j = np.arange(L)
+        blk = self.block_table[s, j // self.bs]
+        slot = j % self.bs
+        K = self.k_pool[blk, :, slot, :]
+        V = self.v_pool[blk, :, :, slot]
+        return K, V
+
+
+# --------------------------------------------------------------------------
+# test-only layer input side
+
+def layer_qkv(x, pos, W_q, W_k, W_v, num_q_heads, num_kv_heads, head_dim,
+              rope_theta=500000.0, rms_eps=1e-5):
+    x = _f64(x)
+    T, d = x.shape
+    pos = _i32(pos)
+    q = np.zeros((T, num_q_heads, head_dim))
+    k = np.zeros((T, num_kv_heads, head_dim))
+    v = np.zeros((T, num_kv_heads, head_dim))
+    lib().orc_layer_qkv(T, d, _ptr(x), _ptr(pos), num_q_heads, num_kv_heads,
+                        head_dim, rope_theta, rms_eps, _ptr(_f64(W_q)),
+                        _ptr(_f64(W_k)), _ptr(_f64(W_v)), _ptr(q), _ptr(k), _ptr(v))
+    return q, k, v

@@ -1,0 +1,86 @@
+/*
+ * oracle.h -- plain, slow, obviously-correct CPU reference of the
+ * span-merging inference hot path, in double precision.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no code,
+ * header, table or helper with the GPU library; the two meet only through
+ * the seeded inputs the tests hand to both.
+ *
+ * Floating inputs arrive as double (bf16 / fp32 values widen exactly);
+ * floating outputs stay double.  Paged-cache pools hold the raw storage
+ * elements (2-byte bf16 or 4-byte fp32 bit patterns) so that copies can be
+ * compared bit for bit.
+ *
+ * Status codes: 0 ok, 1 invalid argument, 2 out of range, 3 out of blocks.
+ * Every cache call validates the whole request list first and changes
+ * nothing when it fails.  Checks run in the order invalid -> range -> memory
+ * and the first class that fails is returned.
+ */
+#ifndef SPANMERGE_ORACLE_H
+#define SPANMERGE_ORACLE_H
+
+#include <stdint.h>
+
+#define ORC_OK 0
+#define ORC_EINVAL 1
+#define ORC_ERANGE 2
+#define ORC_ENOMEM 3
+
+/* Paged cache (element storage: elem_bytes = 2 for bf16, 4 for fp32).
+ *   K page: [num_blocks][num_kv_heads][block_size][head_dim]
+ *   V page: [num_blocks][num_kv_heads][head_dim][block_size]
+ * Cached entry j of sequence s sits in physical block
+ * block_table[s * max_blocks_per_seq + j / block_size], slot j % block_size. */
+typedef struct {
+  int is_bf16;
+  int num_kv_heads, head_dim, block_size, num_blocks, max_seqs,
+      max_blocks_per_seq;
+  void *k_pool, *v_pool;
+  int32_t *block_table, *lengths, *free_stack, *free_top;
+} orc_cache;
+
+/* M_phi over num_spans spans (double everywhere).  flags bit 0: drop GELU,
+ * LayerNorm and biases, which gives the bare form of the main text's Eq. 1. */
+int orc_merge_spans(int d, int h, double ln_eps, const double *emb,
+                    int64_t emb_rows, const int32_t *row_idx,
+                    const int32_t *span_offsets, int num_spans,
+                    const double *Q, const double *W_kv, const double *b_kv,
+                    const double *g_kv, const double *beta_kv,
+                    const double *W_o, const double *b_o, const double *g_o,
+                    const double *beta_o, int flags, double *out,
+                    double *pool_weights /* nullable [num_spans][h][max n] */,
+                    int pool_weights_stride);
+
+int orc_pack_spans(int B, const int32_t *seq_offsets, int num_spans,
+                   const int32_t *span_start, const int32_t *span_len,
+                   const int32_t *seq_span_offsets, int32_t *pi,
+                   int32_t *packed_offsets, int32_t *packed_src,
+                   const int32_t *token_ids, const void *emb,
+                   int64_t emb_rows, const void *surrogates, int d,
+                   int elem_bytes, void *packed /* nullable */);
+
+int orc_kv_rollback(orc_cache *c, const int32_t *seq_ids, const int32_t *k,
+                    int n);
+
+int orc_kv_append(orc_cache *c, const int32_t *seq_ids,
+                  const int32_t *row_offsets, int n, const void *K,
+                  const void *V);
+
+int orc_decode_attention(const orc_cache *c, const int32_t *seq_ids, int n,
+                         const double *q, int num_q_heads, double scale,
+                         double *out, double *probs /* nullable, see .c */,
+                         int probs_stride);
+
+/* Test-only attention-layer input side (not part of the merged path): unit
+ * RMSNorm, then q/k/v projections, rotate-half RoPE at the given positions. */
+void orc_layer_qkv(int T, int d, const double *x, const int32_t *pos,
+                   int num_q_heads, int num_kv_heads, int head_dim,
+                   double rope_theta, double rms_eps, const double *W_q,
+                   const double *W_k, const double *W_v, double *q, double *k,
+                   double *v);
+
+/* Number of OpenMP threads the oracle's parallel loops use. */
+int orc_num_threads(void);
+
+#endif
