@@ -1,0 +1,520 @@
+// Merge module M_phi over many spans at once (gfx950).
+//
+// The module (paper Sec. 3.2 Eq. 1 and the appendix "Attention-based Pooling
+// Architecture") maps the n static embeddings E_s of a span to one surrogate:
+//   P   = LN_kv(GELU(E_s W_kv^T + b_kv))
+//   a_i = softmax_j(P[j, head i] . q_i / sqrt(d_h)),   o_i = sum_j a_i[j] P[j, head i]
+//   z_s = LN_o(GELU([o_1; ...; o_h] W_o^T + b_o))
+//
+// All spans of a call, of any length, are processed together (CSR offsets):
+//   1. GEMM1  G1 = GELU(emb[row_idx] W_kv^T + b_kv)   row-gathered A operand,
+//             bf16 matrix cores (v_mfma_f32_16x16x32_bf16), fp32 accumulate
+//   2. pool   one workgroup per span: exact LN_kv row statistics, the h
+//             head scores, softmax over the span, pooled row c_s
+//   3. GEMM2  Y = GELU(c W_o^T + b_o)                 (fp32 out)
+//   4. LN_o   z_s = LN_o(Y_s)
+// The fp32 dtype runs the same four steps with a vector-ALU GEMM.
+#include "common.hpp"
+
+namespace sm {
+
+// ---------------------------------------------------------------------------
+// bf16 GEMM, C[M][N] = GELU(A[M][K] . B[N][K]^T + bias[N]); A rows optionally
+// gathered through `gather`.  128x128 tile per workgroup, K step 64, four
+// waves each owning a 64x64 quadrant (4x4 MFMA tiles of 16x16).  The next
+// K step is fetched into registers while the current one is multiplied from
+// LDS (double-buffered LDS, one barrier per step).
+
+constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kPitch = kBK + 8;  // bf16 elements per LDS row (16-byte pad)
+
+template <typename OutT>
+__global__ __launch_bounds__(256, 2) void gemm_bf16_nt_gelu(const uint16_t *__restrict__ A,
+                                                            const int32_t *__restrict__ gather,
+                                                            int64_t a_rows, const uint16_t *__restrict__ B,
+                                                            const uint16_t *__restrict__ bias,
+                                                            OutT *__restrict__ C, int M, int N, int K,
+                                                            int32_t *err) {
+  __shared__ uint16_t As[2][kBM * kPitch];
+  __shared__ uint16_t Bs[2][kBN * kPitch];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int r = lane & 15, q4 = lane >> 4;
+  const int n0 = blockIdx.x * kBN, m0 = blockIdx.y * kBM;
+
+  // each thread moves four 16-byte pieces of A and of B per K step
+  const uint16_t *a_src[4];
+  const uint16_t *b_src[4];
+  int lds_off[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int id = tid + 256 * u;
+    const int row = id >> 3, col = (id & 7) * 8;
+    int64_t arow = m0 + row;
+    if (gather) {
+      int gi = (arow < M) ? gather[arow] : 0;
+      if (gi < 0 || gi >= a_rows) {
+        set_err(err, SM_ERR_EINVAL);
+        gi = 0;
+      }
+      arow = gi;
+    } else if (arow >= M) {
+      arow = M - 1;
+    }
+    a_src[u] = A + arow * K + col;
+    b_src[u] = B + (int64_t)(n0 + row) * K + col;
+    lds_off[u] = row * kPitch + col;
+  }
+
+  f32x4_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  u32x4_t ra[4], rb[4];
+  const int nk = K / kBK;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    ra[u] = *(const u32x4_t *)(a_src[u]);
+    rb[u] = *(const u32x4_t *)(b_src[u]);
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    *(u32x4_t *)(&As[0][lds_off[u]]) = ra[u];
+    *(u32x4_t *)(&Bs[0][lds_off[u]]) = rb[u];
+  }
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) {
+      const int ko = (kt + 1) * kBK;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        ra[u] = *(const u32x4_t *)(a_src[u] + ko);
+        rb[u] = *(const u32x4_t *)(b_src[u] + ko);
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < kBK / 32; ++ks) {
+      u32x4_t fa[4], fb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        fa[i] = *(const u32x4_t *)(&As[buf][(wm * 64 + i * 16 + r) * kPitch + ks * 32 + 8 * q4]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        fb[j] = *(const u32x4_t *)(&Bs[buf][(wn * 64 + j * 16 + r) * kPitch + ks * 32 + 8 * q4]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[i]), as_bf16x8(fb[j]), acc[i][j],
+                                                              0, 0, 0);
+    }
+    if (kt + 1 < nk) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        *(u32x4_t *)(&As[buf ^ 1][lds_off[u]]) = ra[u];
+        *(u32x4_t *)(&Bs[buf ^ 1][lds_off[u]]) = rb[u];
+      }
+    }
+    __syncthreads();
+  }
+
+  // epilogue: lane (r, q4) of tile (i, j) holds rows 4*q4 + e, column r
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col = n0 + wn * 64 + j * 16 + r;
+    const float bcol = bf16_to_f32(bias[col]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = m0 + wm * 64 + i * 16 + 4 * q4 + e;
+        if (row < M) {
+          const float v = gelu_erf(acc[i][j][e] + bcol);
+          C[(int64_t)row * N + col] = Elem<OutT>::to_store(v);
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 GEMM on the vector ALU (64x64 tile, 4x4 outputs per thread), same
+// contract as the bf16 one.
+
+constexpr int kFT = 64, kFK = 16;
+
+__global__ __launch_bounds__(256) void gemm_f32_nt_gelu(const float *__restrict__ A,
+                                                        const int32_t *__restrict__ gather, int64_t a_rows,
+                                                        const float *__restrict__ B,
+                                                        const float *__restrict__ bias, float *__restrict__ C,
+                                                        int M, int N, int K, int32_t *err) {
+  __shared__ float As[kFK][kFT + 4];
+  __shared__ float Bs[kFK][kFT + 4];
+  const int tid = threadIdx.x;
+  const int tx = tid & 15, ty = tid >> 4;
+  const int n0 = blockIdx.x * kFT, m0 = blockIdx.y * kFT;
+  // loader: 64 rows x 16 k per operand = 1024 floats, 4 per thread
+  const int lrow = tid >> 2, lk = (tid & 3) * 4;
+  int64_t arow = m0 + lrow;
+  if (gather) {
+    int gi = (arow < M) ? gather[arow] : 0;
+    if (gi < 0 || gi >= a_rows) {
+      set_err(err, SM_ERR_EINVAL);
+      gi = 0;
+    }
+    arow = gi;
+  } else if (arow >= M) {
+    arow = M - 1;
+  }
+  const float *ap = A + arow * K + lk;
+  const float *bp = B + (int64_t)(n0 + lrow) * K + lk;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += kFK) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      As[lk + u][lrow] = ap[k0 + u];
+      Bs[lk + u][lrow] = bp[k0 + u];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kFK; ++kk) {
+      float av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bv[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = m0 + ty * 4 + i;
+    if (row >= M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = n0 + tx * 4 + j;
+      C[(int64_t)row * N + col] = gelu_erf(acc[i][j] + bias[col]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pooling: one workgroup per span.  Thread t owns the 16-byte column groups
+// t, t + 256, ... of every row.
+
+constexpr int kPoolThreads = 256;
+constexpr int kMaxSpanLen = 256;
+constexpr int kMaxHeads = 16;
+constexpr int kMaxD = 8192;
+
+template <typename T>
+struct Vec {
+  static constexpr int N = 16 / sizeof(T);
+};
+
+template <typename T>
+__device__ __forceinline__ void load_vec(const T *p, float *x) {
+  const u32x4_t u = *(const u32x4_t *)p;
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(u[e] << 16);
+      x[2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = __uint_as_float(u[e]);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store_vec(T *p, const float *x) {
+  u32x4_t u;
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) u[e] = pack_bf16x2(x[2 * e], x[2 * e + 1]);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) u[e] = __float_as_uint(x[e]);
+  }
+  *(u32x4_t *)p = u;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kPoolThreads) void pool_kernel(const T *__restrict__ G1,
+                                                            const int32_t *__restrict__ span_offsets,
+                                                            int num_spans, int total_rows,
+                                                            const T *__restrict__ Q, const T *__restrict__ g_kv,
+                                                            const T *__restrict__ beta_kv, float eps, int d,
+                                                            int h, T *__restrict__ cout, int32_t *err) {
+  constexpr int VN = Vec<T>::N;
+  constexpr int kMaxVec = kMaxD / VN / kPoolThreads;
+  __shared__ float red[kPoolThreads / 64][kMaxHeads + 2];
+  __shared__ float row_mean[kMaxSpanLen], row_inv[kMaxSpanLen];
+  __shared__ float alpha[kMaxSpanLen][kMaxHeads];
+  const int s = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int nvec = d / VN;
+  T *dst = cout + (int64_t)s * d;
+
+  const int r0 = span_offsets[s], r1 = span_offsets[s + 1];
+  const int n = r1 - r0;
+  bool ok = n >= 1 && n <= kMaxSpanLen && r0 >= 0 && r1 <= total_rows;
+  if (s == 0 && r0 != 0) ok = false;
+  if (s == num_spans - 1 && r1 != total_rows) ok = false;
+  if (!ok) {
+    if (tid == 0) set_err(err, SM_ERR_EINVAL);
+    const float z[VN] = {};
+    for (int v = tid; v < nvec; v += kPoolThreads) store_vec(dst + v * VN, z);
+    return;
+  }
+  const int dh = d / h;
+  const float inv_sqrt_dh = 1.0f / sqrtf((float)dh);
+
+  // per-thread copies of gamma, beta, q for the owned columns
+  float gv[kMaxVec][VN], bv[kMaxVec][VN], qv[kMaxVec][VN];
+#pragma unroll
+  for (int u = 0; u < kMaxVec; ++u) {
+    const int v = tid + u * kPoolThreads;
+    if (v < nvec) {
+      load_vec(g_kv + v * VN, gv[u]);
+      load_vec(beta_kv + v * VN, bv[u]);
+      load_vec(Q + v * VN, qv[u]);  // Q is [h][d_h] = flat [d]
+    }
+  }
+
+  // pass 1: LN statistics and head scores of every row
+  for (int j = 0; j < n; ++j) {
+    const T *row = G1 + (int64_t)(r0 + j) * d;
+    float x[kMaxVec][VN];
+    float sum = 0.f;
+#pragma unroll
+    for (int u = 0; u < kMaxVec; ++u) {
+      const int v = tid + u * kPoolThreads;
+      if (v < nvec) {
+        load_vec(row + v * VN, x[u]);
+#pragma unroll
+        for (int e = 0; e < VN; ++e) sum += x[u][e];
+      }
+    }
+    const float mean = block_sum(sum, &red[0][0]) / d;
+    float sq = 0.f;
+#pragma unroll
+    for (int u = 0; u < kMaxVec; ++u) {
+      const int v = tid + u * kPoolThreads;
+      if (v < nvec)
+#pragma unroll
+        for (int e = 0; e < VN; ++e) sq += (x[u][e] - mean) * (x[u][e] - mean);
+    }
+    const float var = block_sum(sq, &red[0][0]) / d;
+    const float inv = 1.0f / sqrtf(var + eps);
+    float hs[kMaxHeads];
+#pragma unroll
+    for (int i = 0; i < kMaxHeads; ++i) hs[i] = 0.f;
+#pragma unroll
+    for (int u = 0; u < kMaxVec; ++u) {
+      const int v = tid + u * kPoolThreads;
+      if (v < nvec) {
+        const int head = (v * VN) / dh;  // a 16-byte group never straddles heads
+        float part = 0.f;
+#pragma unroll
+        for (int e = 0; e < VN; ++e) part += (gv[u][e] * (x[u][e] - mean) * inv + bv[u][e]) * qv[u][e];
+#pragma unroll
+        for (int i = 0; i < kMaxHeads; ++i)
+          if (i == head) hs[i] += part;
+      }
+    }
+    __syncthreads();
+    for (int i = 0; i < h; ++i) {
+      const float t = wave_sum(hs[i]);
+      if (lane == 0) red[w][i] = t;
+    }
+    __syncthreads();
+    if (tid < h) {
+      float t = 0.f;
+      for (int ww = 0; ww < kPoolThreads / 64; ++ww) t += red[ww][tid];
+      alpha[j][tid] = t * inv_sqrt_dh;  // raw score for now
+    }
+    if (tid == 0) {
+      row_mean[j] = mean;
+      row_inv[j] = inv;
+    }
+  }
+  __syncthreads();
+  // softmax over the span, per head
+  if (tid < h) {
+    float m = -INFINITY;
+    for (int j = 0; j < n; ++j) m = fmaxf(m, alpha[j][tid]);
+    float z = 0.f;
+    for (int j = 0; j < n; ++j) {
+      const float e = expf(alpha[j][tid] - m);
+      alpha[j][tid] = e;
+      z += e;
+    }
+    const float iz = 1.0f / z;
+    for (int j = 0; j < n; ++j) alpha[j][tid] *= iz;
+  }
+  __syncthreads();
+
+  // pass 2: c = sum_j alpha_j P_j  (rows re-read, L2-resident)
+  float cacc[kMaxVec][VN];
+#pragma unroll
+  for (int u = 0; u < kMaxVec; ++u)
+#pragma unroll
+    for (int e = 0; e < VN; ++e) cacc[u][e] = 0.f;
+  for (int j = 0; j < n; ++j) {
+    const T *row = G1 + (int64_t)(r0 + j) * d;
+    const float mean = row_mean[j], inv = row_inv[j];
+#pragma unroll
+    for (int u = 0; u < kMaxVec; ++u) {
+      const int v = tid + u * kPoolThreads;
+      if (v < nvec) {
+        float x[VN];
+        load_vec(row + v * VN, x);
+        const float a = alpha[j][(v * VN) / dh];
+#pragma unroll
+        for (int e = 0; e < VN; ++e) cacc[u][e] += a * (gv[u][e] * (x[e] - mean) * inv + bv[u][e]);
+      }
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kMaxVec; ++u) {
+    const int v = tid + u * kPoolThreads;
+    if (v < nvec) store_vec(dst + v * VN, cacc[u]);
+  }
+}
+
+// LN_o over fp32 rows Y -> out (storage dtype)
+template <typename T>
+__global__ __launch_bounds__(kPoolThreads) void ln_rows_kernel(const float *__restrict__ Y,
+                                                               const T *__restrict__ g, const T *__restrict__ b,
+                                                               float eps, int d, T *__restrict__ out) {
+  constexpr int kMaxV = kMaxD / 4 / kPoolThreads;
+  __shared__ float red[kPoolThreads / 64];
+  const int s = blockIdx.x, tid = threadIdx.x;
+  const int nvec = d / 4;
+  const float *row = Y + (int64_t)s * d;
+  float x[kMaxV][4];
+  float sum = 0.f;
+#pragma unroll
+  for (int u = 0; u < kMaxV; ++u) {
+    const int v = tid + u * kPoolThreads;
+    if (v < nvec) {
+      load_vec<float>(row + v * 4, x[u]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sum += x[u][e];
+    }
+  }
+  const float mean = block_sum(sum, red) / d;
+  float sq = 0.f;
+#pragma unroll
+  for (int u = 0; u < kMaxV; ++u) {
+    const int v = tid + u * kPoolThreads;
+    if (v < nvec)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sq += (x[u][e] - mean) * (x[u][e] - mean);
+  }
+  const float inv = 1.0f / sqrtf(block_sum(sq, red) / d + eps);
+#pragma unroll
+  for (int u = 0; u < kMaxV; ++u) {
+    const int v = tid + u * kPoolThreads;
+    if (v < nvec) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int col = v * 4 + e;
+        const float gg = Elem<T>::load(g + col), bb = Elem<T>::load(b + col);
+        out[(int64_t)s * d + col] = Elem<T>::to_store(gg * (x[u][e] - mean) * inv + bb);
+      }
+    }
+  }
+}
+
+}  // namespace sm
+
+using namespace sm;
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+SM_API size_t sm_merge_workspace_bytes(int total_rows, int num_spans, int d, sm_dtype dt) {
+  if (total_rows < 0 || num_spans < 0 || d <= 0) return 0;
+  const size_t es = dt == SM_BF16 ? 2 : 4;
+  return align256((size_t)total_rows * d * es) + align256((size_t)num_spans * d * es) +
+         align256((size_t)num_spans * d * 4);
+}
+
+SM_API sm_status sm_merge_spans(const void *emb, int64_t emb_rows, const int32_t *row_idx, int total_rows,
+                                const int32_t *span_offsets, int num_spans, const sm_merge_params *p,
+                                sm_dtype dt, void *out, void *ws, size_t ws_bytes, int32_t *err,
+                                hipStream_t stream) {
+  if (!p || total_rows < 0 || num_spans < 0) return SM_EINVAL;
+  if (dt != SM_F32 && dt != SM_BF16) return SM_EINVAL;
+  const int d = p->d, h = p->h;
+  if (d <= 0 || d > kMaxD || d % 256 != 0 || h <= 0 || h > kMaxHeads || d % h != 0 || (d / h) % 64 != 0)
+    return SM_EINVAL;
+  if (num_spans == 0) return total_rows == 0 ? SM_OK : SM_EINVAL;
+  if (total_rows < num_spans) return SM_EINVAL;
+  if (!emb || emb_rows <= 0 || !row_idx || !span_offsets || !out || !ws || !err) return SM_EINVAL;
+  if (!p->Q || !p->W_kv || !p->b_kv || !p->g_kv || !p->beta_kv || !p->W_o || !p->b_o || !p->g_o ||
+      !p->beta_o)
+    return SM_EINVAL;
+  if (ws_bytes < sm_merge_workspace_bytes(total_rows, num_spans, d, dt)) return SM_EINVAL;
+  if ((total_rows + kBM - 1) / kBM > 65535 || (num_spans + kBM - 1) / kBM > 65535) return SM_EINVAL;
+
+  const size_t es = dt == SM_BF16 ? 2 : 4;
+  char *wsb = (char *)ws;
+  void *g1 = wsb;
+  void *cbuf = wsb + align256((size_t)total_rows * d * es);
+  float *ybuf = (float *)(wsb + align256((size_t)total_rows * d * es) + align256((size_t)num_spans * d * es));
+
+  if (dt == SM_BF16) {
+    hipLaunchKernelGGL(gemm_bf16_nt_gelu<uint16_t>, dim3(d / kBN, (total_rows + kBM - 1) / kBM), dim3(256), 0,
+                       stream, (const uint16_t *)emb, row_idx, emb_rows, (const uint16_t *)p->W_kv,
+                       (const uint16_t *)p->b_kv, (uint16_t *)g1, total_rows, d, d, err);
+    if (hipGetLastError() != hipSuccess) return SM_EHIP;
+    hipLaunchKernelGGL(pool_kernel<uint16_t>, dim3(num_spans), dim3(kPoolThreads), 0, stream,
+                       (const uint16_t *)g1, span_offsets, num_spans, total_rows, (const uint16_t *)p->Q,
+                       (const uint16_t *)p->g_kv, (const uint16_t *)p->beta_kv, p->ln_eps, d, h,
+                       (uint16_t *)cbuf, err);
+    if (hipGetLastError() != hipSuccess) return SM_EHIP;
+    hipLaunchKernelGGL(gemm_bf16_nt_gelu<float>, dim3(d / kBN, (num_spans + kBM - 1) / kBM), dim3(256), 0,
+                       stream, (const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
+                       (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, ybuf, num_spans, d, d, err);
+    if (hipGetLastError() != hipSuccess) return SM_EHIP;
+    hipLaunchKernelGGL(ln_rows_kernel<uint16_t>, dim3(num_spans), dim3(kPoolThreads), 0, stream, ybuf,
+                       (const uint16_t *)p->g_o, (const uint16_t *)p->beta_o, p->ln_eps, d, (uint16_t *)out);
+  } else {
+    hipLaunchKernelGGL(gemm_f32_nt_gelu, dim3(d / kFT, (total_rows + kFT - 1) / kFT), dim3(256), 0, stream,
+                       (const float *)emb, row_idx, emb_rows, (const float *)p->W_kv, (const float *)p->b_kv,
+                       (float *)g1, total_rows, d, d, err);
+    if (hipGetLastError() != hipSuccess) return SM_EHIP;
+    hipLaunchKernelGGL(pool_kernel<float>, dim3(num_spans), dim3(kPoolThreads), 0, stream, (const float *)g1,
+                       span_offsets, num_spans, total_rows, (const float *)p->Q, (const float *)p->g_kv,
+                       (const float *)p->beta_kv, p->ln_eps, d, h, (float *)cbuf, err);
+    if (hipGetLastError() != hipSuccess) return SM_EHIP;
+    hipLaunchKernelGGL(gemm_f32_nt_gelu, dim3(d / kFT, (num_spans + kFT - 1) / kFT), dim3(256), 0, stream,
+                       (const float *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans, (const float *)p->W_o,
+                       (const float *)p->b_o, ybuf, num_spans, d, d, err);
+    if (hipGetLastError() != hipSuccess) return SM_EHIP;
+    hipLaunchKernelGGL(ln_rows_kernel<float>, dim3(num_spans), dim3(kPoolThreads), 0, stream, ybuf,
+                       (const float *)p->g_o, (const float *)p->beta_o, p->ln_eps, d, (float *)out);
+  }
+  return hipGetLastError() == hipSuccess ? SM_OK : SM_EHIP;
+}
+
+SM_API const char *sm_status_string(sm_status s) {
+  switch (s) {
+    case SM_OK: return "ok";
+    case SM_EINVAL: return "invalid argument";
+    case SM_ERANGE: return "length or capacity out of range";
+    case SM_ENOMEM: return "not enough free KV blocks";
+    case SM_EHIP: return "HIP launch failed";
+  }
+  return "unknown status";
+}

@@ -1,0 +1,214 @@
+"""Thin ctypes binding of ``libspanmerge.so`` (argument marshalling only).
+
+Every function mirrors one C entry point of ``include/spanmerge.h`` and takes
+torch tensors that already live on the GPU; the work itself runs in the HIP
+kernels.  There is no CPU fallback: loading fails loudly when the library
+has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libspanmerge.so")
+
+SM_F32, SM_BF16 = 0, 1
+SM_OK, SM_EINVAL, SM_ERANGE, SM_ENOMEM, SM_EHIP = 0, 1, 2, 3, 4
+ERR_EINVAL, ERR_ERANGE, ERR_ENOMEM = 1, 2, 4
+MAX_REQUESTS = 1024
+
+_P, _I, _L, _F, _Z = C.c_void_p, C.c_int, C.c_int64, C.c_float, C.c_size_t
+
+EXPORTED = ("sm_status_string", "sm_merge_workspace_bytes", "sm_merge_spans",
+            "sm_pack_spans", "sm_kv_rollback", "sm_kv_append",
+            "sm_decode_workspace_bytes", "sm_decode_attention")
+
+
+class MergeParams(C.Structure):
+    _fields_ = [("d", _I), ("h", _I), ("ln_eps", _F), ("Q", _P), ("W_kv", _P),
+                ("b_kv", _P), ("g_kv", _P), ("beta_kv", _P), ("W_o", _P),
+                ("b_o", _P), ("g_o", _P), ("beta_o", _P)]
+
+
+class PagedCacheDesc(C.Structure):
+    _fields_ = [("dtype", _I), ("num_kv_heads", _I), ("head_dim", _I),
+                ("block_size", _I), ("num_blocks", _I), ("max_seqs", _I),
+                ("max_blocks_per_seq", _I), ("k_pool", _P), ("v_pool", _P),
+                ("block_table", _P), ("lengths", _P), ("free_stack", _P),
+                ("free_top", _P), ("err", _P)]
+
+
+class SpanMergeError(RuntimeError):
+    pass
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load the HIP library (raises if it is missing: no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise SpanMergeError(
+            f"{path} is missing; build it with `python -m paper_2609_27233_amd.build`")
+    L = C.CDLL(path)
+    L.sm_status_string.argtypes = [_I]
+    L.sm_status_string.restype = C.c_char_p
+    L.sm_merge_workspace_bytes.argtypes = [_I, _I, _I, _I]
+    L.sm_merge_workspace_bytes.restype = _Z
+    L.sm_merge_spans.argtypes = [_P, _L, _P, _I, _P, _I, C.POINTER(MergeParams), _I,
+                                 _P, _P, _Z, _P, _P]
+    L.sm_merge_spans.restype = _I
+    L.sm_pack_spans.argtypes = [_I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _L,
+                                _P, _I, _I, _P, _P, _P]
+    L.sm_pack_spans.restype = _I
+    L.sm_kv_rollback.argtypes = [C.POINTER(PagedCacheDesc), _P, _P, _I, _P]
+    L.sm_kv_rollback.restype = _I
+    L.sm_kv_append.argtypes = [C.POINTER(PagedCacheDesc), _P, _P, _I, _I, _P, _P, _P]
+    L.sm_kv_append.restype = _I
+    L.sm_decode_workspace_bytes.argtypes = [_I, _I, _I, _I]
+    L.sm_decode_workspace_bytes.restype = _Z
+    L.sm_decode_attention.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _I, _F,
+                                      _I, _P, _P, _Z, _P]
+    L.sm_decode_attention.restype = _I
+    _lib = L
+    return L
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise SpanMergeError("expected a GPU tensor")
+    if not t.is_contiguous():
+        raise SpanMergeError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _check(st: int, what: str):
+    if st != SM_OK:
+        msg = load().sm_status_string(st).decode()
+        raise SpanMergeError(f"{what}: {msg} (status {st})")
+
+
+def dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.bfloat16:
+        return SM_BF16
+    if dt == torch.float32:
+        return SM_F32
+    raise SpanMergeError(f"unsupported dtype {dt}")
+
+
+# --------------------------------------------------------------------------
+# merge_spans
+
+def merge_workspace_bytes(total_rows: int, num_spans: int, d: int, dtype: torch.dtype) -> int:
+    return load().sm_merge_workspace_bytes(total_rows, num_spans, d, dtype_code(dtype))
+
+
+def merge_spans(emb, row_idx, span_offsets, params: dict, h: int, out, ws, err,
+                ln_eps: float = 1e-5, total_rows: Optional[int] = None, stream=None):
+    """z_s = M_phi(emb[row_idx[span s]]) for every span; writes ``out``."""
+    S = span_offsets.numel() - 1
+    R = row_idx.numel() if total_rows is None else total_rows
+    p = MergeParams(emb.shape[1], h, ln_eps, *(_ptr(params[k]) for k in
+                    ("Q", "W_kv", "b_kv", "g_kv", "beta_kv", "W_o", "b_o", "g_o", "beta_o")))
+    st = load().sm_merge_spans(_ptr(emb), emb.shape[0], _ptr(row_idx), R,
+                               _ptr(span_offsets), S, C.byref(p), dtype_code(emb.dtype),
+                               _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
+                               _ptr(err), _stream(stream))
+    _check(st, "sm_merge_spans")
+
+
+# --------------------------------------------------------------------------
+# pack_spans
+
+def pack_spans(seq_offsets, span_start, span_len, seq_span_offsets, pi,
+               packed_offsets, packed_src, err, total_tokens: int,
+               token_ids=None, emb=None, surrogates=None, packed=None, stream=None):
+    B = seq_offsets.numel() - 1
+    S = span_start.numel()
+    d = emb.shape[1] if emb is not None else 0
+    dt = dtype_code(emb.dtype) if emb is not None else SM_BF16
+    st = load().sm_pack_spans(B, _ptr(seq_offsets), total_tokens, S, _ptr(span_start),
+                              _ptr(span_len), _ptr(seq_span_offsets), _ptr(pi),
+                              _ptr(packed_offsets), _ptr(packed_src), _ptr(token_ids),
+                              _ptr(emb), emb.shape[0] if emb is not None else 0,
+                              _ptr(surrogates), d, dt, _ptr(packed), _ptr(err),
+                              _stream(stream))
+    _check(st, "sm_pack_spans")
+
+
+# --------------------------------------------------------------------------
+# paged cache
+
+class PagedCache:
+    """Device buffers of one paged KV cache (allocated with torch) and the
+    descriptor the C calls take.  Pools: K [NB, Hkv, bs, D], V [NB, Hkv, D, bs]."""
+
+    def __init__(self, *, dtype: torch.dtype, num_kv_heads: int, head_dim: int,
+                 block_size: int, num_blocks: int, max_seqs: int,
+                 max_blocks_per_seq: int, device="cuda", free_order=None):
+        self.dtype = dtype
+        self.H, self.D, self.bs = num_kv_heads, head_dim, block_size
+        self.num_blocks, self.max_seqs, self.max_blocks = num_blocks, max_seqs, max_blocks_per_seq
+        self.k_pool = torch.zeros((num_blocks, num_kv_heads, block_size, head_dim), dtype=dtype, device=device)
+        self.v_pool = torch.zeros((num_blocks, num_kv_heads, head_dim, block_size), dtype=dtype, device=device)
+        self.block_table = torch.full((max_seqs, max_blocks_per_seq), -1, dtype=torch.int32, device=device)
+        self.lengths = torch.zeros(max_seqs, dtype=torch.int32, device=device)
+        order = (torch.arange(num_blocks, dtype=torch.int32) if free_order is None
+                 else torch.as_tensor(free_order, dtype=torch.int32))
+        # the top of the stack (last element) is handed out first
+        self.free_stack = order.flip(0).contiguous().to(device)
+        self.free_top = torch.tensor([num_blocks], dtype=torch.int32, device=device)
+        self.err = torch.zeros(1, dtype=torch.int32, device=device)
+        self.desc = PagedCacheDesc(dtype_code(dtype), num_kv_heads, head_dim, block_size,
+                                   num_blocks, max_seqs, max_blocks_per_seq,
+                                   _ptr(self.k_pool), _ptr(self.v_pool), _ptr(self.block_table),
+                                   _ptr(self.lengths), _ptr(self.free_stack), _ptr(self.free_top),
+                                   _ptr(self.err))
+
+    def error_bits(self) -> int:
+        return int(self.err.item())
+
+    def clear_error(self):
+        self.err.zero_()
+
+
+def kv_rollback(cache: PagedCache, seq_ids, k, stream=None):
+    st = load().sm_kv_rollback(C.byref(cache.desc), _ptr(seq_ids), _ptr(k), seq_ids.numel(),
+                               _stream(stream))
+    _check(st, "sm_kv_rollback")
+
+
+def kv_append(cache: PagedCache, seq_ids, row_offsets, K, V, total_rows: Optional[int] = None,
+              stream=None):
+    R = K.shape[0] if total_rows is None else total_rows
+    st = load().sm_kv_append(C.byref(cache.desc), _ptr(seq_ids), _ptr(row_offsets),
+                             seq_ids.numel(), R, _ptr(K), _ptr(V), _stream(stream))
+    _check(st, "sm_kv_append")
+
+
+def decode_workspace_bytes(n: int, num_q_heads: int, head_dim: int, max_len: int) -> int:
+    return load().sm_decode_workspace_bytes(n, num_q_heads, head_dim, max_len)
+
+
+def decode_attention(cache: PagedCache, seq_ids, q, out, ws, max_len: int,
+                     scale: Optional[float] = None, stream=None):
+    n, Hq, D = q.shape
+    sc = D ** -0.5 if scale is None else scale
+    st = load().sm_decode_attention(C.byref(cache.desc), _ptr(seq_ids), n, _ptr(q), Hq, sc,
+                                    max_len, _ptr(out), _ptr(ws),
+                                    ws.numel() * ws.element_size(), _stream(stream))
+    _check(st, "sm_decode_attention")

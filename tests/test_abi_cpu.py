@@ -1,0 +1,97 @@
+"""The C ABI library loads and exports every declared symbol; host-side
+argument checks return their status without touching a GPU."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from conftest import ROOT
+from paper_2609_27233_amd import lib as sm
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "spanmerge.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(sm_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return sm.load()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _declared()
+    assert set(names) == set(sm.EXPORTED)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_no_other_exports():
+    # symbols are hidden by default; only the sm_ entry points are visible
+    out = os.popen("nm -D --defined-only %s" % sm.LIB_PATH).read()
+    exported = {ln.split()[-1] for ln in out.splitlines() if " T " in ln}
+    assert {n for n in exported if n.startswith("sm_")} == set(sm.EXPORTED)
+
+
+def test_status_strings(L):
+    assert L.sm_status_string(0) == b"ok"
+    assert b"argument" in L.sm_status_string(1)
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    saved = sm._lib
+    sm._lib = None
+    try:
+        with pytest.raises(sm.SpanMergeError):
+            sm.load(str(tmp_path / "nope.so"))
+    finally:
+        sm._lib = saved
+
+
+def _desc(**kw):
+    base = dict(dtype=sm.SM_BF16, num_kv_heads=8, head_dim=128, block_size=16, num_blocks=64,
+                max_seqs=4, max_blocks_per_seq=16, k_pool=1, v_pool=1, block_table=1,
+                lengths=1, free_stack=1, free_top=1, err=1)
+    base.update(kw)
+    return sm.PagedCacheDesc(*base.values())
+
+
+@pytest.mark.parametrize("kw", [dict(head_dim=96), dict(block_size=24), dict(block_size=8),
+                                dict(dtype=7), dict(k_pool=None), dict(num_blocks=0)])
+def test_cache_descriptor_checks(L, kw):
+    d = _desc(**kw)
+    assert L.sm_kv_rollback(C.byref(d), 1, 1, 1, None) == sm.SM_EINVAL
+    assert L.sm_kv_append(C.byref(d), 1, 1, 1, 1, 1, 1, None) == sm.SM_EINVAL
+    assert L.sm_decode_attention(C.byref(d), 1, 1, 1, 8, 1.0, 16, 1, 1, 1 << 30, None) == sm.SM_EINVAL
+
+
+def test_request_count_and_workspace_checks(L):
+    d = _desc()
+    assert L.sm_kv_rollback(C.byref(d), 1, 1, 5, None) == sm.SM_EINVAL       # n > max_seqs
+    assert L.sm_kv_rollback(C.byref(d), 1, 1, 0, None) == sm.SM_OK           # nothing to do
+    assert L.sm_decode_attention(C.byref(d), 1, 1, 1, 12, 1.0, 16, 1, 1, 1 << 30, None) == sm.SM_EINVAL  # Hq % Hkv
+    assert L.sm_decode_attention(C.byref(d), 1, 1, 1, 8 * 17, 1.0, 16, 1, 1, 1 << 30, None) == sm.SM_EINVAL  # G > 16
+    need = L.sm_decode_workspace_bytes(1, 32, 128, 256)
+    assert need > 0
+    assert L.sm_decode_attention(C.byref(d), 1, 1, 1, 32, 1.0, 256, 1, 1, need - 1, None) == sm.SM_EINVAL
+    assert L.sm_decode_attention(C.byref(d), 1, 1, 1, 32, 1.0, 257, 1, 1, 1 << 30, None) == sm.SM_EINVAL  # > capacity
+
+
+def test_merge_argument_checks(L):
+    p = sm.MergeParams(4096, 4, 1e-5, *([1] * 9))
+    ws = L.sm_merge_workspace_bytes(100, 30, 4096, sm.SM_BF16)
+    assert ws >= 100 * 4096 * 2 + 30 * 4096 * 6
+    assert L.sm_merge_spans(1, 10, 1, 100, 1, 30, C.byref(p), sm.SM_BF16, 1, 1, ws - 1, 1, None) == sm.SM_EINVAL
+    bad = sm.MergeParams(4000, 4, 1e-5, *([1] * 9))   # d % 256 != 0
+    assert L.sm_merge_spans(1, 10, 1, 100, 1, 30, C.byref(bad), sm.SM_BF16, 1, 1, 1 << 40, 1, None) == sm.SM_EINVAL
+    assert L.sm_merge_spans(1, 10, 1, 10, 1, 30, C.byref(p), sm.SM_BF16, 1, 1, 1 << 40, 1, None) == sm.SM_EINVAL  # rows < spans
+    assert L.sm_merge_spans(1, 10, 1, 0, 1, 0, C.byref(p), sm.SM_BF16, 1, 1, 0, 1, None) == sm.SM_OK
+
+
+def test_pack_argument_checks(L):
+    assert L.sm_pack_spans(-1, 1, 0, 0, 1, 1, 1, 1, 1, 1, None, None, 0, None, 0, 1, None, 1, None) == sm.SM_EINVAL
+    assert L.sm_pack_spans(0, 1, 0, 0, 1, 1, 1, 1, 1, 1, None, None, 0, None, 0, 1, None, 1, None) == sm.SM_OK
+    # rows requested without an embedding table
+    assert L.sm_pack_spans(2, 1, 8, 1, 1, 1, 1, 1, 1, 1, None, None, 0, None, 64, 1, 1, 1, None) == sm.SM_EINVAL

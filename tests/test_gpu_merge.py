@@ -1,0 +1,112 @@
+"""GPU merge_spans (M_phi) vs the oracle."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import TOL, dev, i32, rel_l2_max, say
+from paper_2609_27233_amd import lib as sm
+from paper_2609_27233_amd import workload as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_merge(emb, row_idx, offs, params, h, dtype):
+    S = len(offs) - 1
+    d = emb.shape[1]
+    out = torch.full((S, d), float("nan"), dtype=dtype, device=dev())
+    ws = torch.empty(sm.merge_workspace_bytes(len(row_idx), S, d, dtype), dtype=torch.uint8, device=dev())
+    err = torch.zeros(1, dtype=torch.int32, device=dev())
+    pd = {k: v.to(dev()) for k, v in params.items()}
+    sm.merge_spans(emb, i32(row_idx), i32(offs), pd, h, out, ws, err)
+    torch.cuda.synchronize()
+    return out.cpu(), int(err.item())
+
+
+def _oracle(orc, emb_rows_f64, row_idx, offs, params, h, sample=None):
+    if sample is None:
+        st, ref = orc.merge_spans(emb_rows_f64, row_idx, offs, {k: wl.to_f64(v) for k, v in params.items()}, h)
+        assert st == orc.OK
+        return ref
+    # re-pack the sampled spans as their own CSR list
+    rows = np.concatenate([row_idx[offs[s]:offs[s + 1]] for s in sample])
+    so = np.concatenate([[0], np.cumsum([offs[s + 1] - offs[s] for s in sample])]).astype(np.int32)
+    st, ref = orc.merge_spans(emb_rows_f64, rows, so, {k: wl.to_f64(v) for k, v in params.items()}, h)
+    assert st == orc.OK
+    return ref
+
+
+@pytest.mark.parametrize("spread", [False, True])
+def test_merge_tiny_f32(orc, spread):
+    w = wl.WORKLOADS[1]
+    P = wl.make_prompts(w)
+    g = wl.generator(w.seed)
+    emb = wl.randn((w.vocab, w.d), torch.float32, g, std=0.02)
+    params = wl.make_merge_params(w.d, w.h, torch.float32, g, spread=spread)
+    say("merge f32 tiny spread", spread, "spans", len(P.span_len))
+    out, err = _gpu_merge(emb.to(dev()), P.row_idx, P.span_offsets, params, w.h, torch.float32)
+    assert err == 0
+    ref = _oracle(orc, wl.to_f64(emb), P.row_idx, P.span_offsets, params, w.h)
+    e = rel_l2_max(out.numpy(), ref)
+    say("rel_l2_max", e)
+    assert e <= TOL[torch.float32]
+
+
+@pytest.mark.parametrize("d,S,nmax,spread", [(512, 300, 8, True), (1024, 129, 5, False),
+                                             (768, 37, 12, True), (256, 1, 1, True)])
+def test_merge_bf16_small(orc, d, S, nmax, spread):
+    rng = np.random.RandomState(d + S)
+    lens = rng.randint(1, nmax + 1, size=S)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    vocab = 2000
+    row_idx = rng.randint(0, vocab, size=int(offs[-1])).astype(np.int32)
+    g = wl.generator(d)
+    emb = wl.randn((vocab, d), torch.bfloat16, g, std=0.02)
+    params = wl.make_merge_params(d, 4, torch.bfloat16, g, spread=spread)
+    say("merge bf16", d, S, nmax, spread)
+    out, err = _gpu_merge(emb.to(dev()), row_idx, offs, params, 4, torch.bfloat16)
+    assert err == 0
+    ref = _oracle(orc, wl.to_f64(emb), row_idx, offs, params, 4)
+    e = rel_l2_max(out.float().numpy(), ref)
+    say("rel_l2_max", e)
+    assert e <= TOL[torch.bfloat16]
+
+
+def test_merge_llama3_8b_prompt_batch(orc):
+    """All ~9.7k spans of the 16 x 4096 workload in one call on the GPU; a
+    seeded sample of spans checked against the oracle."""
+    w = wl.WORKLOADS[2]
+    P = wl.make_prompts(w)
+    g = wl.generator(w.seed, "cuda")
+    emb = wl.randn((w.vocab, w.d), torch.bfloat16, g, device="cuda", std=0.02)
+    params = wl.make_merge_params(w.d, w.h, torch.bfloat16, g, device="cuda")
+    S = len(P.span_len)
+    say("merge llama3-8b prompts, spans", S, "rows", len(P.row_idx))
+    out, err = _gpu_merge(emb, P.row_idx, P.span_offsets, params, w.h, torch.bfloat16)
+    assert err == 0
+    rng = np.random.RandomState(0)
+    sample = np.sort(rng.choice(S, size=24, replace=False))
+    sample = np.unique(np.concatenate([sample, [0, S - 1]]))
+    used = np.unique(np.concatenate([P.row_idx[P.span_offsets[s]:P.span_offsets[s + 1]] for s in sample]))
+    # the oracle gets the used rows only (remapped), exact float64 copies
+    remap = {int(r): i for i, r in enumerate(used)}
+    emb_used = wl.to_f64(emb[torch.as_tensor(used, device="cuda")])
+    sub_rows = np.concatenate([[remap[int(r)] for r in P.row_idx[P.span_offsets[s]:P.span_offsets[s + 1]]]
+                               for s in sample]).astype(np.int32)
+    so = np.concatenate([[0], np.cumsum([P.span_offsets[s + 1] - P.span_offsets[s] for s in sample])]).astype(np.int32)
+    st, ref = orc.merge_spans(emb_used, sub_rows, so, {k: wl.to_f64(v) for k, v in params.items()}, w.h)
+    assert st == orc.OK
+    e = rel_l2_max(out[torch.as_tensor(sample)].float().numpy(), ref)
+    say("rel_l2_max over", len(sample), "spans:", e)
+    assert e <= TOL[torch.bfloat16]
+    assert torch.isfinite(out.float()).all()
+
+
+def test_merge_bad_row_index_sets_einval(orc):
+    d = 256
+    g = wl.generator(3)
+    emb = wl.randn((10, d), torch.bfloat16, g)
+    params = wl.make_merge_params(d, 4, torch.bfloat16, g)
+    say("merge bad row index")
+    out, err = _gpu_merge(emb.to(dev()), np.array([1, 2, 99], np.int32), np.array([0, 2, 3], np.int32),
+                          params, 4, torch.bfloat16)
+    assert err == sm.ERR_EINVAL
