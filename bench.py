@@ -1,0 +1,369 @@
+#!/usr/bin/env python
+"""Benchmark of the span-merging inference hot path on one MI355X.
+
+Workload: one Llama-3-8B-shaped attention layer (d = 4096, 32 query / 8 KV
+heads, head_dim 128, bf16), batch 16, 4096-token prompts compressed by span
+merging (spans of 2-8 tokens, 40% effective-length reduction -> 2458 cached
+entries per sequence), then 256 decode steps.  Every 8th decode step each
+sequence merges a freshly completed span of n = 2..4 tokens (merge module ->
+roll back n-1 entries -> append the surrogate's K/V); the other steps append
+the new token's K/V.  Every step ends with decode attention over the
+compacted paged cache (16-token pages).
+
+One benchmark step runs that whole job for R resident batches ("replicas")
+of 16 sequences, served round-robin the way a server alternates between
+batches; R * (bytes per attention launch) is several times the 256 MB
+Infinity Cache, so no attention launch finds its KV in the MALL.
+
+Printed: one JSON line with the whole-job decode throughput, the decode
+attention kernel's achieved HBM bandwidth against the 8 TB/s roofline
+(measured live with HIP events on the launch stream around each decode
+step's back-to-back attention launches), and the CPU oracle timed on a
+bounded sample of the same job.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+METRIC = "decode-attention tokens/s + achieved HBM GB/s over span-compacted KV cache"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class Job:
+    """Device state of R resident batches of one workload."""
+
+    def __init__(self, w, R, dev, seed_base=0):
+        import torch
+        from paper_2609_27233_amd import lib as sm
+        from paper_2609_27233_amd import workload as wl
+
+        self.w, self.R, self.dev = w, R, dev
+        self.sm, self.L = sm, sm.load()
+        bf = w.torch_dtype
+        B, H, D, Hq, bs = w.batch, w.num_kv_heads, w.head_dim, w.num_q_heads, w.block_size
+        T = w.prompt_len
+        g = wl.generator(w.seed + seed_base, dev)
+        t0 = time.time()
+        self.emb = wl.randn((w.vocab, w.d), bf, g, device=dev, std=0.02)
+        self.params = wl.make_merge_params(w.d, w.h, bf, g, device=dev)
+        i32 = lambda a: torch.as_tensor(np.asarray(a, np.int32)).to(dev)
+
+        self.prompts = [wl.make_prompts(w, seed=w.seed + 97 * r + seed_base) for r in range(R)]
+        self.dev_prompts = []
+        for P in self.prompts:
+            self.dev_prompts.append(dict(
+                row_idx=i32(P.row_idx), span_offsets=i32(P.span_offsets), seq_offsets=i32(P.seq_offsets),
+                span_start=i32(P.span_start), span_len=i32(P.span_len),
+                seq_span_offsets=i32(P.seq_span_offsets), token_ids=i32(P.token_ids),
+                S=len(P.span_len), rows=len(P.row_idx)))
+        removed = [int(np.sum(P.span_len - 1)) for P in self.prompts]
+        self.packed_rows = [B * T - r for r in removed]
+        self.L0 = T - int(round(w.target * T))          # cached entries per sequence after compression
+        assert all(pr == B * self.L0 for pr in self.packed_rows)
+
+        steps = w.decode_steps
+        self.max_len = self.L0 + steps
+        nb_seq = -(-self.max_len // bs) + 2
+        self.caches = [sm.PagedCache(dtype=bf, num_kv_heads=H, head_dim=D, block_size=bs,
+                                     num_blocks=B * nb_seq, max_seqs=B, max_blocks_per_seq=nb_seq,
+                                     device=dev) for _ in range(R)]
+        Smax = max(p["S"] for p in self.dev_prompts)
+        rows_max = max(p["rows"] for p in self.dev_prompts)
+        self.z = torch.empty((Smax, w.d), dtype=bf, device=dev)
+        self.merge_ws = torch.empty(sm.merge_workspace_bytes(rows_max, Smax, w.d, bf), dtype=torch.uint8, device=dev)
+        self.err = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.pi = torch.empty(B * T, dtype=torch.int32, device=dev)
+        self.po = torch.empty(B + 1, dtype=torch.int32, device=dev)
+        self.ps = torch.empty(B * T, dtype=torch.int32, device=dev)
+        self.packed = torch.empty((B * T, w.d), dtype=bf, device=dev)
+        # prompt K/V (what the frozen backbone would produce for the packed rows)
+        self.Kp = wl.randn((self.packed_rows[0], H, D), bf, g, device=dev)
+        self.Vp = wl.randn((self.packed_rows[0], H, D), bf, g, device=dev)
+        # per-step inputs, cycled
+        self.nin = 16
+        self.Kt = [wl.randn((B, H, D), bf, g, device=dev) for _ in range(self.nin)]
+        self.Vt = [wl.randn((B, H, D), bf, g, device=dev) for _ in range(self.nin)]
+        self.q = [wl.randn((B, Hq, D), bf, g, device=dev) for _ in range(self.nin)]
+        self.out = torch.empty((B, Hq, D), dtype=bf, device=dev)
+        self.dec_ws = torch.zeros(sm.decode_workspace_bytes(B, Hq, D, self.max_len), dtype=torch.uint8, device=dev)
+        self.ids = i32(np.arange(B))
+        self.one_row = i32(np.arange(B + 1))
+        self.kreset = torch.empty(B, dtype=torch.int32, device=dev)
+        # decode-time merges: n per sequence per merge step, spans drawn from
+        # a synthetic generated-token stream
+        self.merge_steps = [s for s in range(steps) if w.merge_every and s % w.merge_every == w.merge_every - 1]
+        rng = np.random.RandomState(w.seed + 5)
+        self.dmerge = {}
+        for s in self.merge_steps:
+            n = wl.decode_merge_lengths(w, s)
+            offs = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+            self.dmerge[s] = dict(n=n, k=i32(n - 1), offs=i32(offs), rows=int(offs[-1]),
+                                  row_idx=i32(rng.randint(0, w.vocab, size=int(offs[-1]))))
+        self.zdec = torch.empty((B, w.d), dtype=bf, device=dev)
+        self.dmerge_ws = torch.empty(sm.merge_workspace_bytes(B * max(w.merge_n), B, w.d, bf),
+                                     dtype=torch.uint8, device=dev)
+        # host-side copy of the length schedule (for the algorithmic bytes)
+        self.len_sched = []
+        lens = np.full(B, self.L0, np.int64)
+        for s in range(steps):
+            if s in self.dmerge:
+                lens = lens - (self.dmerge[s]["n"] - 1) + 1
+            else:
+                lens = lens + 1
+            self.len_sched.append(lens.copy())
+        torch.cuda.synchronize()
+        self._prep_ctypes()
+        log(f"setup {time.time() - t0:.1f}s: R={R}, spans/batch={Smax}, packed rows/batch={self.packed_rows[0]}, "
+            f"L0={self.L0}, max_len={self.max_len}")
+
+    def _prep_ctypes(self):
+        sm = self.sm
+        w = self.w
+        p = self.params
+        self.mp = sm.MergeParams(w.d, w.h, 1e-5, *(p[k].data_ptr() for k in
+                                 ("Q", "W_kv", "b_kv", "g_kv", "beta_kv", "W_o", "b_o", "g_o", "beta_o")))
+        self.descs = [C.byref(c.desc) for c in self.caches]
+
+    def decode_bytes(self, lens):
+        """Algorithmic HBM bytes of one attention launch over lengths `lens`:
+        K and V of every cached entry, the queries, the outputs and the block
+        table entries read."""
+        w = self.w
+        es = 2
+        kv = 2 * int(np.sum(lens)) * w.num_kv_heads * w.head_dim * es
+        qo = 2 * w.batch * w.num_q_heads * w.head_dim * es
+        bt = 4 * int(np.sum(-(-lens // w.block_size)))
+        return kv + qo + bt
+
+    def run(self, stream, events=None):
+        """One benchmark step: the whole job for every resident batch."""
+        import torch
+        L, sm, w = self.L, self.sm, self.w
+        B = w.batch
+        st = stream.cuda_stream
+        bf = sm.SM_BF16
+        for r in range(self.R):
+            c, dp = self.caches[r], self.dev_prompts[r]
+            # evict the previous job's sequences (rollback of everything)
+            self.kreset.copy_(c.lengths[:B])
+            rc = L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), self.kreset.data_ptr(), B, st)
+            # prompt compression: merge every span, pack, bulk-append the prompt K/V
+            rc |= L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], dp["row_idx"].data_ptr(), dp["rows"],
+                                   dp["span_offsets"].data_ptr(), dp["S"], C.byref(self.mp), bf,
+                                   self.z.data_ptr(), self.merge_ws.data_ptr(), self.merge_ws.numel(),
+                                   self.err.data_ptr(), st)
+            rc |= L.sm_pack_spans(B, dp["seq_offsets"].data_ptr(), B * w.prompt_len, dp["S"],
+                                  dp["span_start"].data_ptr(), dp["span_len"].data_ptr(),
+                                  dp["seq_span_offsets"].data_ptr(), self.pi.data_ptr(), self.po.data_ptr(),
+                                  self.ps.data_ptr(), dp["token_ids"].data_ptr(), self.emb.data_ptr(),
+                                  self.emb.shape[0], self.z.data_ptr(), w.d, bf, self.packed.data_ptr(),
+                                  self.err.data_ptr(), st)
+            rc |= L.sm_kv_append(self.descs[r], self.ids.data_ptr(), self.po.data_ptr(), B, self.packed_rows[r],
+                                 self.Kp.data_ptr(), self.Vp.data_ptr(), st)
+            if rc:
+                raise RuntimeError(f"prompt compression launch failed: {rc}")
+        for s in range(w.decode_steps):
+            j = s % self.nin
+            m = self.dmerge.get(s)
+            rc = 0
+            # every batch first updates its cache: a decode-time merge (merge
+            # module, roll back n-1 entries, append the surrogate's K/V) or
+            # the new token's K/V ...
+            for r in range(self.R):
+                d = self.descs[r]
+                if m is not None:
+                    rc |= L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], m["row_idx"].data_ptr(), m["rows"],
+                                           m["offs"].data_ptr(), B, C.byref(self.mp), bf, self.zdec.data_ptr(),
+                                           self.dmerge_ws.data_ptr(), self.dmerge_ws.numel(), self.err.data_ptr(), st)
+                    rc |= L.sm_kv_rollback(d, self.ids.data_ptr(), m["k"].data_ptr(), B, st)
+                rc |= L.sm_kv_append(d, self.ids.data_ptr(), self.one_row.data_ptr(), B, B,
+                                     self.Kt[j].data_ptr(), self.Vt[j].data_ptr(), st)
+            # ... then the attention launches of all batches run back to back
+            if events is not None:
+                events[0][s].record(stream)
+            for r in range(self.R):
+                rc |= L.sm_decode_attention(self.descs[r], self.ids.data_ptr(), B, self.q[j].data_ptr(),
+                                            w.num_q_heads, w.head_dim ** -0.5, self.max_len, self.out.data_ptr(),
+                                            self.dec_ws.data_ptr(), self.dec_ws.numel(), st)
+            if events is not None:
+                events[1][s].record(stream)
+            if rc:
+                raise RuntimeError(f"decode launch failed at step {s}: {rc}")
+
+    def check_errors(self):
+        bits = [c.error_bits() for c in self.caches] + [int(self.err.item())]
+        if any(bits):
+            raise RuntimeError(f"device error bits set: {bits}")
+
+
+def cpu_baseline(job, target_s=20.0):
+    """Time the oracle on a bounded sample of one batch's job and scale it to
+    the whole job.  Sample: M_phi on 32 of the prompt spans (scaled to all
+    spans), pack + bulk append of one batch's prompt, and 2 decode steps
+    (append + attention) at the starting length (scaled to 256 steps)."""
+    import torch
+    import oracle as orc
+    from paper_2609_27233_amd import workload as wl
+
+    w = job.w
+    B, H, D, Hq = w.batch, w.num_kv_heads, w.head_dim, w.num_q_heads
+    P = job.prompts[0]
+    S = len(P.span_len)
+    t_all = time.time()
+    # merge module on a sample of spans
+    ns = 1024
+    sample = np.arange(ns) * (S // ns)
+    offs = P.span_offsets
+    rows = np.concatenate([P.row_idx[offs[s]:offs[s + 1]] for s in sample])
+    uniq, inv = np.unique(rows, return_inverse=True)
+    emb_s = wl.to_f64(job.emb[torch.as_tensor(uniq, device=job.dev)])
+    so = np.concatenate([[0], np.cumsum([offs[s + 1] - offs[s] for s in sample])]).astype(np.int32)
+    params = {k: wl.to_f64(v) for k, v in job.params.items()}
+    t = time.time()
+    st, _ = orc.merge_spans(emb_s, inv.astype(np.int32), so, params, w.h)
+    t_merge = (time.time() - t) * S / ns
+    assert st == 0
+    # pack of the whole batch (indices) and bulk append of its K/V
+    t = time.time()
+    st, res = orc.pack_spans(P.seq_offsets, P.span_start, P.span_len, P.seq_span_offsets)
+    t_pack = time.time() - t
+    nb_seq = -(-job.max_len // w.block_size) + 2
+    oc = orc.OracleCache(bf16=True, num_kv_heads=H, head_dim=D, block_size=w.block_size,
+                         num_blocks=B * nb_seq, max_seqs=B, max_blocks_per_seq=nb_seq)
+    Kp, Vp = wl.to_raw(job.Kp), wl.to_raw(job.Vp)
+    t = time.time()
+    st = oc.append(np.arange(B), res["packed_offsets"], Kp, Vp)
+    t_append = time.time() - t
+    assert st == 0
+    # decode steps
+    nd = 24
+    Kt, Vt = wl.to_raw(job.Kt[0]), wl.to_raw(job.Vt[0])
+    q = wl.to_f64(job.q[0])
+    t = time.time()
+    for _ in range(nd):
+        oc.append(np.arange(B), np.arange(B + 1), Kt, Vt)
+        oc.decode_attention(np.arange(B), q, Hq, D ** -0.5)
+    t_dec = (time.time() - t) / nd
+    # attention cost grows with the cache: scale by the mean length over the job
+    mean_len = float(np.mean([np.mean(x) for x in job.len_sched]))
+    t_dec_job = t_dec * w.decode_steps * mean_len / (job.L0 + 1)
+    t_job = t_merge + t_pack + t_append + t_dec_job
+    tokens = B * w.decode_steps
+    return {
+        "value": tokens / t_job,
+        "unit": "tokens/s",
+        "cores": orc.num_threads(),
+        "kind": "oracle",
+        "sample": (f"fp64 oracle on one 16-sequence batch: M_phi on {ns} of {S} prompt spans "
+                   f"(scaled x{S / ns:.0f}), full pack and bulk append ({job.packed_rows[0]} rows), "
+                   f"{nd} decode steps scaled to {w.decode_steps} by mean cache length; "
+                   f"job estimate {t_job:.1f}s from {time.time() - t_all:.1f}s measured"),
+        "seconds_measured": round(time.time() - t_all, 2),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--replicas", type=int, default=8)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build measures the single-GPU hot path "
+              f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_27233_amd import workload as wl
+
+    dev = torch.device("cuda:0")
+    w = wl.WORKLOADS[2]
+    job = Job(w, args.replicas, dev)
+    stream = torch.cuda.current_stream()
+    nlaunch = w.decode_steps * job.R
+
+    for i in range(args.warmup):
+        job.run(stream)
+        torch.cuda.synchronize()
+        log(f"warmup {i} done")
+    job.check_errors()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(w.decode_steps)] for _ in range(2)]
+    attn_ms = 0.0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        job.run(stream, events=ev)
+        torch.cuda.synchronize()
+        attn_ms += sum(a.elapsed_time(b) for a, b in zip(ev[0], ev[1]))
+        log(f"step {i} done")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    job.check_errors()
+
+    ms_per_step = elapsed * 1e3 / args.steps
+    tokens = job.R * w.batch * w.decode_steps
+    value = tokens * args.steps / elapsed
+    bytes_per_step = sum(job.decode_bytes(l) for l in job.len_sched) * job.R
+    avg_launch_us = attn_ms * 1e3 / (nlaunch * args.steps)
+    achieved = bytes_per_step * args.steps / (attn_ms * 1e-3) / 1e9
+    mean_bytes = bytes_per_step / nlaunch
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{w.name}: 40% span-merged prompts (L0={job.L0}), {w.decode_steps} decode steps, "
+                        f"decode-time merge every {w.merge_every} steps, {job.R} resident batches",
+            "batch": w.batch, "prompt_len": w.prompt_len, "compacted_len": job.L0,
+            "decode_steps": w.decode_steps, "resident_batches": job.R,
+            "layer": {"d": w.d, "q_heads": w.num_q_heads, "kv_heads": w.num_kv_heads, "head_dim": w.head_dim},
+            "block_size": w.block_size,
+        },
+        "roofline": {
+            "kernel": "decode_split_bf16<128>: one launch per decode step and batch; HIP events around "
+                      "each step's back-to-back launches, divided by the launch count",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": None,
+            "avg_launch_us": round(avg_launch_us, 3),
+            "algorithmic_bytes_per_launch": int(mean_bytes),
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(job)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

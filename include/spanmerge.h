@@ -109,7 +109,8 @@ typedef struct {
  *
  * Entry j of sequence s lives in block block_table[s][j / block_size] at
  * slot j % block_size.  head_dim must be 64 or 128; block_size must be a
- * power of two in [16, 512].
+ * power of two in [16, 512]; num_kv_heads * head_dim <= 2048.  Pools must
+ * be 16-byte aligned.
  */
 typedef struct {
   sm_dtype dtype;
@@ -264,8 +265,9 @@ size_t sm_decode_workspace_bytes(int n, int num_q_heads, int head_dim,
  *   out[i, h] = sum_j softmax_j(scale * q[i, h] . K[s, j, g]) V[s, j, g]
  *   s = seq_ids[i],  g = h / (num_q_heads / num_kv_heads)   (grouped query)
  *
- * A sequence of length 0 gives zeros.  Implemented as split-K (partials
- * over chunks of the cache) followed by an exact combine.
+ * A sequence of length 0 gives zeros.  Implemented as one kernel: split-K
+ * partials over chunks of the cache, combined exactly by the last workgroup
+ * of each (sequence, kv head) to finish.
  *
  *  seq_ids      [n] ids in [0, max_seqs) (repeats allowed)
  *  q            [n][num_q_heads][head_dim] (cache dtype)
@@ -273,7 +275,11 @@ size_t sm_decode_workspace_bytes(int n, int num_q_heads, int head_dim,
  *  max_len      (host) upper bound on lengths[seq_ids[i]]; sizes the grid
  *  out          [n][num_q_heads][head_dim] (cache dtype)
  *  ws, ws_bytes at least sm_decode_workspace_bytes(n, num_q_heads,
- *               head_dim, max_len)
+ *               head_dim, max_len).  Its first 256 KiB hold arrival
+ *               counters: zero-fill them once before the first call; every
+ *               call leaves them zero again, so one workspace serves calls
+ *               of any shape.  Calls that may run concurrently must not
+ *               share a workspace.  n * num_kv_heads <= 65536.
  * Device errors (into c->err; the affected rows are zero): EINVAL (bad id,
  * block id out of range), ERANGE (length > max_len).
  */

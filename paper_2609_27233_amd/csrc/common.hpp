@@ -123,4 +123,24 @@ __device__ __forceinline__ void set_err(int32_t *err, int bit) {
   atomicOr(err, bit);
 }
 
+
+// Division by a runtime divisor d (1 <= d < 2^31) for 0 <= x < 2^31 as a
+// multiply-high and shift (Granlund & Montgomery, "Division by invariant
+// integers using multiplication", PLDI 1994): shift = ceil(log2 d),
+// mul = floor(2^32 (2^shift - d) / d) + 1, q = (mulhi(x, mul) + x) >> shift.
+struct FastDiv {
+  uint32_t d, mul, shift;
+};
+
+static inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t sh = 0;
+  while ((1ull << sh) < d) ++sh;
+  const uint64_t m = ((1ull << 32) * ((1ull << sh) - d)) / d + 1;
+  return FastDiv{d, (uint32_t)m, sh};
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t x, const FastDiv &f) {
+  return (__umulhi(x, f.mul) + x) >> f.shift;
+}
+
 }  // namespace sm

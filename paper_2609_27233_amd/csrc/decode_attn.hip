@@ -12,8 +12,10 @@
 // by exactly one MFMA), compute S^T = K Q^T and O^T += V^T P^T with
 // v_mfma_f32_16x16x32_bf16 (the G query heads of the group padded to 16
 // columns), and keep an online softmax per head.  The waves merge through
-// LDS and write one unnormalised partial (O, m, l) per chunk.
-// Phase 2 (combine): rescale and sum the partials exactly.
+// LDS and write one unnormalised partial (O, m, l) per chunk.  The last
+// workgroup of a (sequence, kv head) to finish -- found with an arrival
+// counter in the workspace -- rescales and sums the partials exactly and
+// writes the output, so one kernel launch does the whole operation.
 //
 // V pages are stored dim-major ([head_dim][block_size]), so the 8 tokens a
 // lane feeds to the PV product are 16 contiguous bytes.  The QK rows of the
@@ -41,18 +43,20 @@ struct DecodeArgs {
   void *out;
   float *ws_o;   // [n][Hq][max_chunks][DH]
   float *ws_ml;  // [n][Hq][max_chunks][2]
+  int32_t *counters;  // [n][Hkv] arrival counters, zero between calls
   int32_t *err;
   int Hkv, Hq, G, bs_log2, num_blocks, max_seqs, max_blocks;
   int chunk_nominal, max_chunks, max_len;
   float scale_log2e;
 };
 
-// Chunking of a sequence of L cached entries: nc chunks of `chunk` tokens
-// (a multiple of 32), all of nearly equal size.  Split and combine both call
-// this with the same L, so they agree on the partials that exist.
+// Chunking of a sequence of L cached entries: nc non-empty chunks of
+// `chunk` tokens (a multiple of 32, at most C), all of nearly equal size.
+// Every workgroup of the sequence computes the same split from the same L.
 __device__ __forceinline__ void chunking(int L, int C, int &nc, int &chunk) {
-  nc = (L + C - 1) / C;
-  chunk = nc ? ((L + nc - 1) / nc + 31) / 32 * 32 : 0;
+  const int n0 = (L + C - 1) / C;
+  chunk = n0 ? ((L + n0 - 1) / n0 + 31) / 32 * 32 : 0;
+  nc = chunk ? (L + chunk - 1) / chunk : 0;
 }
 
 // Sequence-level checks shared by split and combine.  Returns 0 when the
@@ -84,14 +88,72 @@ __device__ __forceinline__ bool load_pages(const DecodeArgs &a, int s, int lp0,
   return *flag == 0;
 }
 
+// Partials travel between workgroups as device-scope ("agent") relaxed
+// atomic stores and loads: on gfx950 these go through the coherent level of
+// the memory hierarchy, so no cache-wide writeback/invalidate fence is
+// needed (such fences cost more than the whole attention pass).  Every
+// store a workgroup makes has completed before its thread 0 bumps the
+// arrival counter (the barrier waits for outstanding memory operations).
+__device__ __forceinline__ void put_partial(float *p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float get_partial(const float *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ void write_bad_partial(const DecodeArgs &a, int i,
                                                   int g, int c) {
   if (threadIdx.x < a.G) {
     const int64_t pidx = ((int64_t)i * a.Hq + g * a.G + threadIdx.x) * a.max_chunks + c;
-    a.ws_ml[pidx * 2 + 0] = 0.f;
-    a.ws_ml[pidx * 2 + 1] = -1.f;  // marks the chunk as unusable
+    put_partial(&a.ws_ml[pidx * 2 + 0], 0.f);
+    put_partial(&a.ws_ml[pidx * 2 + 1], -1.f);  // marks the chunk as unusable
   }
   if (threadIdx.x == 0) set_err(a.err, SM_ERR_EINVAL);
+}
+
+// Zero the output rows of group g's query heads (done by the chunk-0
+// workgroup of a sequence that cannot be processed or is empty) and report a
+// sequence-level error.
+template <typename OutT>
+__device__ void write_zero_rows(const DecodeArgs &a, int i, int g, int DH, int st) {
+  OutT *o = (OutT *)a.out + ((int64_t)i * a.Hq + g * a.G) * DH;
+  for (int e = threadIdx.x; e < a.G * DH; e += blockDim.x) o[e] = Elem<OutT>::to_store(0.f);
+  if (st != 0 && threadIdx.x == 0) set_err(a.err, st);
+}
+
+// Every workgroup calls this once its partial is stored.  The last of the
+// nc workgroups of (sequence i, kv head g) to arrive rescales and sums all
+// partials of the group, writes the output rows and re-arms the counter.
+template <typename OutT>
+__device__ void finish_group(const DecodeArgs &a, int i, int g, int nc, int DH, int *last) {
+  int32_t *ctr = a.counters + (int64_t)i * a.Hkv + g;
+  __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores are done
+  __syncthreads();
+  if (threadIdx.x == 0)
+    *last = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nc - 1;
+  __syncthreads();
+  if (!*last) return;
+  OutT *out = (OutT *)a.out;
+  for (int e = threadIdx.x; e < a.G * DH; e += blockDim.x) {
+    const int hh = e / DH, dd = e - hh * DH;
+    const int64_t base = ((int64_t)i * a.Hq + g * a.G + hh) * a.max_chunks;
+    float M = -INFINITY;
+    bool bad = false;
+    for (int c = 0; c < nc; ++c) {
+      bad |= get_partial(&a.ws_ml[(base + c) * 2 + 1]) < 0.f;
+      M = fmaxf(M, get_partial(&a.ws_ml[(base + c) * 2 + 0]));
+    }
+    float acc = 0.f, ls = 0.f;
+    if (!bad) {
+      for (int c = 0; c < nc; ++c) {
+        const float f = exp2f(get_partial(&a.ws_ml[(base + c) * 2 + 0]) - M);
+        acc += get_partial(&a.ws_o[(base + c) * DH + dd]) * f;
+        ls += get_partial(&a.ws_ml[(base + c) * 2 + 1]) * f;
+      }
+    }
+    out[((int64_t)i * a.Hq + g * a.G + hh) * DH + dd] = Elem<OutT>::to_store(bad ? 0.f : acc / ls);
+  }
+  if (threadIdx.x == 0) *ctr = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -116,17 +178,22 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int s = a.seq_ids[i];
   int L;
-  if (seq_status(a, s, L) != 0 || L == 0) return;  // combine reports it
+  const int st = seq_status(a, s, L);
+  if (st != 0 || L == 0) {
+    if (c == 0) write_zero_rows<uint16_t>(a, i, g, DH, st);
+    return;
+  }
   int nc, chunk;
   chunking(L, a.chunk_nominal, nc, chunk);
+  if (c >= nc) return;
   const int t0 = c * chunk;
-  if (c >= nc || t0 >= L) return;
   const int t1 = min(L, t0 + chunk);
   const int bs_log2 = a.bs_log2, bs = 1 << bs_log2;
   const int lp0 = t0 >> bs_log2;
   const int npages = ((t1 - 1) >> bs_log2) - lp0 + 1;
   if (!load_pages(a, s, lp0, npages, pages, &flag)) {
     write_bad_partial(a, i, g, c);
+    finish_group<uint16_t>(a, i, g, nc, DH, &flag);
     return;
   }
 
@@ -166,11 +233,12 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     const uint16_t *pV = vp + ((int64_t)bV * a.Hkv + g) * page_elems + (int64_t)r * bs + (tV & (bs - 1));
 #pragma unroll
     for (int kk = 0; kk < DH / 32; ++kk) {
-      T.ka[kk] = *(const u32x4_t *)(pA + 32 * kk);
-      T.kb[kk] = *(const u32x4_t *)(pB + 32 * kk);
+      T.ka[kk] = __builtin_nontemporal_load((const u32x4_t *)(pA + 32 * kk));
+      T.kb[kk] = __builtin_nontemporal_load((const u32x4_t *)(pB + 32 * kk));
     }
 #pragma unroll
-    for (int dt = 0; dt < DH / 16; ++dt) T.v[dt] = *(const u32x4_t *)(pV + (int64_t)16 * dt * bs);
+    for (int dt = 0; dt < DH / 16; ++dt)
+      T.v[dt] = __builtin_nontemporal_load((const u32x4_t *)(pV + (int64_t)16 * dt * bs));
   };
 
   f32x4_t o[DH / 16];
@@ -228,13 +296,17 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
       o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(T.v[dt]), as_bf16x8(pp), o[dt], 0, 0, 0);
   };
 
-  KVTile<DH> cur, nxt;
-  int tile = w;
-  if (tile < ntiles) load(cur, tile);
-  for (; tile < ntiles; tile += kDecWaves) {
-    if (tile + kDecWaves < ntiles) load(nxt, tile + kDecWaves);
-    compute(cur, tile);
-    cur = nxt;
+  // two register buffers, alternating without copies: while one tile is
+  // multiplied the next one's 16 loads are in flight
+  KVTile<DH> bufA, bufB;
+  constexpr int step = kDecWaves;
+  if (w < ntiles) load(bufA, w);
+  for (int tile = w; tile < ntiles; tile += 2 * step) {
+    if (tile + step < ntiles) load(bufB, tile + step);
+    compute(bufA, tile);
+    if (tile + step >= ntiles) break;
+    if (tile + 2 * step < ntiles) load(bufA, tile + 2 * step);
+    compute(bufB, tile + step);
   }
 
   // per-head totals of this wave (lanes r, r+16, r+32, r+48 share head r)
@@ -262,13 +334,18 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
       acc += red_o[ww][hh][dd] * f;
       ls += red_l[ww][hh] * f;
     }
+    if (nc == 1) {  // the only chunk: write the result directly
+      ((uint16_t *)a.out)[((int64_t)i * a.Hq + g * G + hh) * DH + dd] = f32_to_bf16(acc / ls);
+      continue;
+    }
     const int64_t pidx = ((int64_t)i * a.Hq + g * G + hh) * a.max_chunks + c;
-    a.ws_o[pidx * DH + dd] = acc;
+    put_partial(&a.ws_o[pidx * DH + dd], acc);
     if (dd == 0) {
-      a.ws_ml[pidx * 2 + 0] = M;
-      a.ws_ml[pidx * 2 + 1] = ls;
+      put_partial(&a.ws_ml[pidx * 2 + 0], M);
+      put_partial(&a.ws_ml[pidx * 2 + 1], ls);
     }
   }
+  if (nc > 1) finish_group<uint16_t>(a, i, g, nc, DH, &flag);
 }
 
 // ---------------------------------------------------------------------------
@@ -289,17 +366,22 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_f32(DecodeArgs a) {
   const int tid = threadIdx.x;
   const int s = a.seq_ids[i];
   int L;
-  if (seq_status(a, s, L) != 0 || L == 0) return;
+  const int st = seq_status(a, s, L);
+  if (st != 0 || L == 0) {
+    if (c == 0) write_zero_rows<float>(a, i, g, DH, st);
+    return;
+  }
   int nc, chunk;
   chunking(L, a.chunk_nominal, nc, chunk);
+  if (c >= nc) return;
   const int t0 = c * chunk;
-  if (c >= nc || t0 >= L) return;
   const int t1 = min(L, t0 + chunk);
   const int bs_log2 = a.bs_log2, bs = 1 << bs_log2;
   const int lp0 = t0 >> bs_log2;
   const int npages = ((t1 - 1) >> bs_log2) - lp0 + 1;
   if (!load_pages(a, s, lp0, npages, pages, &flag)) {
     write_bad_partial(a, i, g, c);
+    finish_group<float>(a, i, g, nc, DH, &flag);
     return;
   }
   const float *kp = (const float *)a.k_pool;
@@ -342,54 +424,15 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_f32(DecodeArgs a) {
       float o = 0.f;
       for (int k = 0; k < NG; ++k) o += opart[k][tid];
       const int64_t pidx = ((int64_t)i * a.Hq + hq) * a.max_chunks + c;
-      a.ws_o[pidx * DH + tid] = o;
+      put_partial(&a.ws_o[pidx * DH + tid], o);
       if (tid == 0) {
-        a.ws_ml[pidx * 2 + 0] = M;
-        a.ws_ml[pidx * 2 + 1] = l;
+        put_partial(&a.ws_ml[pidx * 2 + 0], M);
+        put_partial(&a.ws_ml[pidx * 2 + 1], l);
       }
     }
     __syncthreads();
   }
-}
-
-// ---------------------------------------------------------------------------
-// combine: one workgroup of head_dim threads per (query head, sequence)
-
-template <typename OutT>
-__global__ void decode_combine(DecodeArgs a, int DH) {
-  const int h = blockIdx.x, i = blockIdx.y, dd = threadIdx.x;
-  OutT *out = (OutT *)a.out + ((int64_t)i * a.Hq + h) * DH + dd;
-  const int s = a.seq_ids[i];
-  int L;
-  const int st = seq_status(a, s, L);
-  if (st != 0 || L == 0) {
-    if (st != 0 && dd == 0) set_err(a.err, st);
-    *out = Elem<OutT>::to_store(0.f);
-    return;
-  }
-  int nc, chunk;
-  chunking(L, a.chunk_nominal, nc, chunk);
-  const int64_t base = ((int64_t)i * a.Hq + h) * a.max_chunks;
-  float M = -INFINITY;
-  bool bad = false;
-  for (int c = 0; c < nc; ++c) {
-    if (c * chunk >= L) break;
-    const float l = a.ws_ml[(base + c) * 2 + 1];
-    if (l < 0.f) bad = true;
-    M = fmaxf(M, a.ws_ml[(base + c) * 2 + 0]);
-  }
-  if (bad) {
-    *out = Elem<OutT>::to_store(0.f);
-    return;
-  }
-  float acc = 0.f, ls = 0.f;
-  for (int c = 0; c < nc; ++c) {
-    if (c * chunk >= L) break;
-    const float f = exp2f(a.ws_ml[(base + c) * 2 + 0] - M);
-    acc += a.ws_o[(base + c) * DH + dd] * f;
-    ls += a.ws_ml[(base + c) * 2 + 1] * f;
-  }
-  *out = Elem<OutT>::to_store(acc / ls);
+  finish_group<float>(a, i, g, nc, DH, &flag);
 }
 
 }  // namespace sm
@@ -404,20 +447,27 @@ static int ilog2_exact(int v) {
 }
 
 static int chunk_policy_bf16(int n, int Hkv, int max_len) {
-  // Enough chunks that the grid fills the chip once (two 4-wave workgroups
-  // per compute unit), each chunk a multiple of 128 tokens (32 per wave).
-  const int64_t slots = 512;
-  int64_t c = ((int64_t)max_len * n * Hkv + slots - 1) / slots;
+  // One workgroup per compute unit when every sequence is at max_len (long
+  // contiguous streams per workgroup measured fastest), with chunks kept
+  // between 256 and 2048 tokens so that batches of mixed lengths still
+  // split into enough pieces to balance; a multiple of 128 tokens (32 per
+  // wave).
+  const int64_t cus = 256;
+  int64_t c = ((int64_t)max_len * n * Hkv + cus - 1) / cus;
   c = (c + 127) / 128 * 128;
-  if (c < 128) c = 128;
-  if (c > kMaxChunkTokens) c = kMaxChunkTokens;
+  if (c < 256) c = 256;
+  if (c > 2048) c = 2048;
   return (int)c;
 }
+
+// Workspace layout: [arrival counters, kCounterBytes][partial O][partial m, l]
+constexpr int64_t kCounterBytes = 256 * 1024;
+constexpr int64_t kMaxPairs = kCounterBytes / 4;  // n * num_kv_heads
 
 SM_API size_t sm_decode_workspace_bytes(int n, int num_q_heads, int head_dim, int max_len) {
   if (n <= 0 || num_q_heads <= 0 || head_dim <= 0 || max_len < 0) return 0;
   const int64_t max_chunks = (max_len + 127) / 128 + 1;  // any chunk size >= 128
-  return (size_t)((int64_t)n * num_q_heads * max_chunks * (head_dim + 2) * sizeof(float));
+  return (size_t)(kCounterBytes + (int64_t)n * num_q_heads * max_chunks * (head_dim + 2) * sizeof(float));
 }
 
 SM_API sm_status sm_decode_attention(const sm_paged_cache *c, const int32_t *seq_ids, int n,
@@ -437,7 +487,7 @@ SM_API sm_status sm_decode_attention(const sm_paged_cache *c, const int32_t *seq
   if (G > 16) return SM_EINVAL;
   if (c->num_blocks <= 0 || c->max_seqs <= 0 || c->max_blocks_per_seq <= 0) return SM_EINVAL;
   if ((int64_t)max_len > (int64_t)c->max_blocks_per_seq * c->block_size) return SM_EINVAL;
-  if (n > 65535) return SM_EINVAL;
+  if (n > 65535 || (int64_t)n * c->num_kv_heads > kMaxPairs) return SM_EINVAL;
   if (ws_bytes < sm_decode_workspace_bytes(n, num_q_heads, c->head_dim, max_len)) return SM_EINVAL;
 
   DecodeArgs a;
@@ -461,29 +511,23 @@ SM_API sm_status sm_decode_attention(const sm_paged_cache *c, const int32_t *seq
                                           : kF32ChunkTokens;
   a.max_chunks = max_len > 0 ? (max_len + a.chunk_nominal - 1) / a.chunk_nominal : 1;
   a.scale_log2e = scale * kLog2e;
-  a.ws_o = (float *)ws;
+  a.counters = (int32_t *)ws;
+  a.ws_o = (float *)((char *)ws + kCounterBytes);
   a.ws_ml = a.ws_o + (int64_t)n * num_q_heads * a.max_chunks * c->head_dim;
 
-  if (max_len > 0) {
-    dim3 grid(a.max_chunks, c->num_kv_heads, n);
-    if (c->dtype == SM_BF16) {
-      if (c->head_dim == 128)
-        hipLaunchKernelGGL(decode_split_bf16<128>, grid, dim3(kDecThreads), 0, stream, a);
-      else
-        hipLaunchKernelGGL(decode_split_bf16<64>, grid, dim3(kDecThreads), 0, stream, a);
-    } else {
-      if (c->head_dim == 128)
-        hipLaunchKernelGGL(decode_split_f32<128>, grid, dim3(kDecThreads), 0, stream, a);
-      else
-        hipLaunchKernelGGL(decode_split_f32<64>, grid, dim3(kDecThreads), 0, stream, a);
-    }
-    if (hipGetLastError() != hipSuccess) return SM_EHIP;
+  // one launch: split, and the last workgroup of each (sequence, kv head)
+  // combines; with max_len = 0 the single chunk column writes zero rows
+  const dim3 grid(a.max_chunks, c->num_kv_heads, n);
+  if (c->dtype == SM_BF16) {
+    if (c->head_dim == 128)
+      hipLaunchKernelGGL(decode_split_bf16<128>, grid, dim3(kDecThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL(decode_split_bf16<64>, grid, dim3(kDecThreads), 0, stream, a);
+  } else {
+    if (c->head_dim == 128)
+      hipLaunchKernelGGL(decode_split_f32<128>, grid, dim3(kDecThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL(decode_split_f32<64>, grid, dim3(kDecThreads), 0, stream, a);
   }
-  dim3 cgrid(num_q_heads, n);
-  if (c->dtype == SM_BF16)
-    hipLaunchKernelGGL(decode_combine<uint16_t>, cgrid, dim3(c->head_dim), 0, stream, a, c->head_dim);
-  else
-    hipLaunchKernelGGL(decode_combine<float>, cgrid, dim3(c->head_dim), 0, stream, a, c->head_dim);
-  if (hipGetLastError() != hipSuccess) return SM_EHIP;
-  return SM_OK;
+  return hipGetLastError() == hipSuccess ? SM_OK : SM_EHIP;
 }

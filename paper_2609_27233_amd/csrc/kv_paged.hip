@@ -24,7 +24,7 @@ struct CacheArgs {
   int32_t *free_stack;
   int32_t *free_top;
   int32_t *err;
-  int Hkv, DH, bs_log2, num_blocks, max_seqs, max_blocks;
+  int Hkv, DH, dh_log2, bs_log2, num_blocks, max_seqs, max_blocks;
 };
 
 constexpr int kMetaThreads = 1024;
@@ -102,35 +102,173 @@ __global__ __launch_bounds__(kMetaThreads) void rollback_kernel(CacheArgs c, con
   if (t == 0) *c.free_top = top + total;
 }
 
-__global__ __launch_bounds__(kMetaThreads) void append_meta_kernel(CacheArgs c, const int32_t *seq_ids,
-                                                                    const int32_t *row_offsets, int n,
-                                                                    int total_rows) {
-  __shared__ int red[16];
-  __shared__ int fl_inval, fl_range, fl_stack, s_err, s_top;
+// Validation and block allocation of kv_append, run by one workgroup of
+// kMetaThreads threads (thread t owns request t).  Returns true, uniformly
+// across the workgroup, when the call was applied; on return *L_old holds
+// request t's length before the call.
+struct AppendShared {
+  int red[16];
+  int fl_inval, fl_range, fl_stack, s_err, s_top;
+};
+
+__device__ bool append_meta_body(const CacheArgs &c, const int32_t *seq_ids, const int32_t *row_offsets, int n,
+                                 int total_rows, AppendShared &sh, int &s_out, int &L_old) {
   const int t = threadIdx.x;
   if (t == 0) {
-    fl_inval = 0;
-    fl_range = 0;
-    fl_stack = 0;
-    s_err = *c.err;
-    s_top = *c.free_top;
-    if (row_offsets[0] != 0 || row_offsets[n] != total_rows) fl_inval = 1;
+    sh.fl_inval = 0;
+    sh.fl_range = 0;
+    sh.fl_stack = 0;
+    sh.s_err = *c.err;
+    sh.s_top = *c.free_top;
+    if (row_offsets[0] != 0 || row_offsets[n] != total_rows) sh.fl_inval = 1;
   }
   __syncthreads();
-  if (s_err != 0) return;
+  if (sh.s_err != 0) return false;  // sticky: the cache is frozen
 
   const bool active = t < n;
   int s = 0, m = 0;
   if (active) {
     s = seq_ids[t];
     m = row_offsets[t + 1] - row_offsets[t];
-    if (m < 0 || !id_ok(seq_ids, t, s, c.max_seqs)) fl_inval = 1;
+    if (m < 0 || !id_ok(seq_ids, t, s, c.max_seqs)) sh.fl_inval = 1;
+  }
+  __syncthreads();
+  if (sh.fl_inval) {
+    if (t == 0) set_err(c.err, SM_ERR_EINVAL);
+    return false;
+  }
+  const int cap = c.max_blocks << c.bs_log2;
+  int L = 0, need = 0;
+  if (active) {
+    L = c.lengths[s];
+    if (L < 0 || (int64_t)L + m > cap) sh.fl_range = 1;
+    else need = blocks_for(L + m, c.bs_log2) - blocks_for(L, c.bs_log2);
+  }
+  __syncthreads();
+  if (sh.fl_range) {
+    if (t == 0) set_err(c.err, SM_ERR_ERANGE);
+    return false;
+  }
+  int total;
+  const int incl = block_inclusive_scan(need, sh.red, &total);
+  const int top = sh.s_top;
+  if (top < 0 || top > c.num_blocks || total > top) {
+    if (t == 0) set_err(c.err, SM_ERR_ENOMEM);
+    return false;
+  }
+  // every id about to be popped must name a real block
+  for (int j = t; j < total; j += blockDim.x) {
+    const int blk = c.free_stack[top - 1 - j];
+    if (blk < 0 || blk >= c.num_blocks) sh.fl_stack = 1;
+  }
+  __syncthreads();
+  if (sh.fl_stack) {
+    if (t == 0) set_err(c.err, SM_ERR_EINVAL);
+    return false;
+  }
+  if (active) {
+    int32_t *row = c.block_table + (int64_t)s * c.max_blocks;
+    const int first = blocks_for(L, c.bs_log2);
+    const int pop0 = incl - need;  // pops already taken by earlier requests
+    for (int q = 0; q < need; ++q) row[first + q] = c.free_stack[top - 1 - (pop0 + q)];
+    c.lengths[s] = L + m;
+  }
+  if (t == 0) *c.free_top = top - total;
+  s_out = s;
+  L_old = L;
+  return true;
+}
+
+__global__ __launch_bounds__(kMetaThreads) void append_meta_kernel(CacheArgs c, const int32_t *seq_ids,
+                                                                    const int32_t *row_offsets, int n,
+                                                                    int total_rows) {
+  __shared__ AppendShared sh;
+  int s, L;
+  append_meta_body(c, seq_ids, row_offsets, n, total_rows, sh, s, L);
+}
+
+// Copy rows [r_begin, r_end) of K and V into their slots; row_blk/row_slot
+// (LDS) give the destination of row r - r_begin (block -1: skip).  One unit
+// = one 16-byte group of one row (VEC elements of one head); `upr` divides
+// by the units per row.  Threads `lane0`, lane0 + stride, ... share the
+// units; each unit's K and V loads are issued before its stores.
+template <typename T>
+__device__ __forceinline__ void copy_rows(const CacheArgs &c, const T *__restrict__ K, const T *__restrict__ V,
+                                          int r_begin, int r_end, const FastDiv &upr, const int *row_blk,
+                                          const int *row_slot, int lane0, int stride) {
+  constexpr int VEC = 16 / sizeof(T);
+  const int bs = 1 << c.bs_log2;
+  const int gpl2 = c.dh_log2 - (sizeof(T) == 2 ? 3 : 2);  // log2(groups per head)
+  const int row_elems = c.Hkv << c.dh_log2;
+  const int units = (r_end - r_begin) * (int)upr.d;
+  T *kp = (T *)c.k_pool;
+  T *vp = (T *)c.v_pool;
+  for (int u = lane0; u < units; u += stride) {
+    const int rr = (int)fdiv((uint32_t)u, upr);
+    const int gi = u - rr * (int)upr.d;           // group within the row
+    const int g = gi >> gpl2, d0 = (gi & ((1 << gpl2) - 1)) * VEC;
+    const int64_t src = (int64_t)(r_begin + rr) * row_elems + (int64_t)gi * VEC;
+    const u32x4_t kv = *(const u32x4_t *)(K + src);
+    const u32x4_t vv = *(const u32x4_t *)(V + src);
+    const int blk = row_blk[rr];
+    if (blk < 0) continue;
+    const int slot = row_slot[rr];
+    *(u32x4_t *)(kp + (((int64_t)blk * c.Hkv + g) * bs + slot) * c.DH + d0) = kv;
+    T *vdst = vp + (((int64_t)blk * c.Hkv + g) * c.DH + d0) * bs + slot;
+    const T *ve = (const T *)&vv;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) vdst[e * bs] = ve[e];
+  }
+}
+
+// Small appends (a decode step: one row per sequence) in ONE workgroup,
+// metadata and copy together.  The sequence of dependent global accesses is
+// kept short: (1) ids / offsets / error word, (2) lengths, (3) the tail
+// block of each sequence and the popped free-stack entries, (4) the row
+// copies.  Same validation order and block order as the two-kernel path.
+constexpr int kSmallBytes = 64 * 1024;  // of K (and of V) per call
+constexpr int kSmallRows = 1024;
+
+template <typename T>
+__global__ __launch_bounds__(kMetaThreads) void append_small_kernel(CacheArgs c, const int32_t *seq_ids,
+                                                                     const int32_t *row_offsets, int n,
+                                                                     int total_rows, const T *__restrict__ K,
+                                                                     const T *__restrict__ V, FastDiv upr) {
+  __shared__ int red[16];
+  __shared__ int ids[kMetaThreads];
+  __shared__ int fl_inval, fl_range, fl_stack, s_err, s_top;
+  __shared__ int row_blk[kSmallRows], row_slot[kSmallRows];
+  const int t = threadIdx.x;
+  const bool active = t < n;
+  // (1)
+  int s = -1, r0 = 0, r1 = 0;
+  if (active) {
+    s = seq_ids[t];
+    r0 = row_offsets[t];
+    r1 = row_offsets[t + 1];
+    ids[t] = s;
+  }
+  if (t == 0) {
+    fl_range = 0;
+    fl_stack = 0;
+    s_err = *c.err;
+    s_top = *c.free_top;
+    fl_inval = (row_offsets[0] != 0 || row_offsets[n] != total_rows);
+  }
+  __syncthreads();
+  if (s_err != 0) return;  // sticky: the cache is frozen
+  if (active) {
+    bool ok = r1 >= r0 && s >= 0 && s < c.max_seqs;
+    for (int j = 0; j < t && ok; ++j) ok = ids[j] != s;
+    if (!ok) fl_inval = 1;
   }
   __syncthreads();
   if (fl_inval) {
     if (t == 0) set_err(c.err, SM_ERR_EINVAL);
     return;
   }
+  // (2)
+  const int m = r1 - r0;
   const int cap = c.max_blocks << c.bs_log2;
   int L = 0, need = 0;
   if (active) {
@@ -150,24 +288,42 @@ __global__ __launch_bounds__(kMetaThreads) void append_meta_kernel(CacheArgs c, 
     if (t == 0) set_err(c.err, SM_ERR_ENOMEM);
     return;
   }
-  // every id about to be popped must name a real block
+  // (3) every popped id must name a real block; the partially filled tail
+  // block (if a new row lands in it) is read once
   for (int j = t; j < total; j += kMetaThreads) {
     const int blk = c.free_stack[top - 1 - j];
     if (blk < 0 || blk >= c.num_blocks) fl_stack = 1;
   }
+  int32_t *brow = c.block_table + (int64_t)(active ? s : 0) * c.max_blocks;
+  const int first = blocks_for(L, c.bs_log2);  // first logical block to allocate
+  const int lp_tail = L >> c.bs_log2;           // page of the first new row
+  const int tail_blk = (active && m > 0 && lp_tail < first) ? brow[lp_tail] : -1;
   __syncthreads();
   if (fl_stack) {
     if (t == 0) set_err(c.err, SM_ERR_EINVAL);
     return;
   }
+  const int bs = 1 << c.bs_log2;
   if (active) {
-    int32_t *row = c.block_table + (int64_t)s * c.max_blocks;
-    const int first = blocks_for(L, c.bs_log2);
     const int pop0 = incl - need;  // pops already taken by earlier requests
-    for (int q = 0; q < need; ++q) row[first + q] = c.free_stack[top - 1 - (pop0 + q)];
+    for (int q = 0; q < need; ++q) brow[first + q] = c.free_stack[top - 1 - (pop0 + q)];
     c.lengths[s] = L + m;
+    for (int r = r0; r < r1; ++r) {
+      const int pos = L + (r - r0);
+      const int lp = pos >> c.bs_log2;
+      const int b = (lp < first) ? tail_blk : c.free_stack[top - 1 - (pop0 + lp - first)];
+      const bool ok = b >= 0 && b < c.num_blocks;
+      if (!ok) set_err(c.err, SM_ERR_EINVAL);  // corrupt block table
+      row_blk[r] = ok ? b : -1;
+      row_slot[r] = pos & (bs - 1);
+    }
   }
   if (t == 0) *c.free_top = top - total;
+  __syncthreads();
+  // (4) the copy, in units of one 16-byte group of one row: the K group
+  // goes to its token-major page with one 16-byte store, the V group's
+  // elements go to the dim-major page one slot at a time
+  copy_rows<T>(c, K, V, 0, total_rows, upr, row_blk, row_slot, t, kMetaThreads);
 }
 
 // Copy phase of kv_append: 16 consecutive input rows per workgroup.  K rows
@@ -176,11 +332,13 @@ __global__ __launch_bounds__(kMetaThreads) void append_meta_kernel(CacheArgs c, 
 // consecutive slots.
 constexpr int kCopyRows = 16;
 constexpr int kCopyThreads = 256;
+constexpr int kMaxRowElems = 2048;  // num_kv_heads * head_dim
 
 template <typename T>
 __global__ __launch_bounds__(kCopyThreads) void append_copy_kernel(CacheArgs c, const int32_t *seq_ids,
                                                                    const int32_t *row_offsets, int n,
-                                                                   int total_rows, const T *K, const T *V) {
+                                                                   int total_rows, const T *__restrict__ K,
+                                                                   const T *__restrict__ V) {
   extern __shared__ unsigned char smem_raw[];
   T *vs = reinterpret_cast<T *>(smem_raw);  // [kCopyRows][row_elems + pad]
   __shared__ int row_blk[kCopyRows], row_slot[kCopyRows];
@@ -228,15 +386,29 @@ __global__ __launch_bounds__(kCopyThreads) void append_copy_kernel(CacheArgs c, 
     for (int u = 0; u < VEC; ++u) vs[rr * pitch + cc + u] = src[u];
   }
   __syncthreads();
-  // K rows: 16-byte vector copies into token-major pages
+  // K rows: 16-byte vector copies into token-major pages, all loads of a
+  // thread issued before its stores
   T *kp = (T *)c.k_pool;
-  for (int e = t; e < nrows * vpr; e += kCopyThreads) {
-    const int rr = e / vpr, cc = (e - rr * vpr) * VEC;
-    const int blk = row_blk[rr];
-    if (blk < 0) continue;
-    const int g = cc / c.DH, d = cc - g * c.DH;
-    const u32x4_t val = *(const u32x4_t *)(K + (int64_t)(r0 + rr) * row_elems + cc);
-    *(u32x4_t *)(kp + (((int64_t)blk * c.Hkv + g) * bs + row_slot[rr]) * c.DH + d) = val;
+  constexpr int KP = kCopyRows * (kMaxRowElems / VEC) / kCopyThreads;
+  u32x4_t kr[KP];
+#pragma unroll
+  for (int u = 0; u < KP; ++u) {
+    const int e = t + u * kCopyThreads;
+    if (e < nrows * vpr) {
+      const int rr = e / vpr, cc = (e - rr * vpr) * VEC;
+      kr[u] = *(const u32x4_t *)(K + (int64_t)(r0 + rr) * row_elems + cc);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < KP; ++u) {
+    const int e = t + u * kCopyThreads;
+    if (e < nrows * vpr) {
+      const int rr = e / vpr, cc = (e - rr * vpr) * VEC;
+      const int blk = row_blk[rr];
+      if (blk < 0) continue;
+      const int g = cc / c.DH, d = cc - g * c.DH;
+      *(u32x4_t *)(kp + (((int64_t)blk * c.Hkv + g) * bs + row_slot[rr]) * c.DH + d) = kr[u];
+    }
   }
   // V rows: transposed element stores, slot (row) fastest
   T *vp = (T *)c.v_pool;
@@ -429,6 +601,7 @@ static bool cache_ok(const sm_paged_cache *c, CacheArgs &a) {
   a.err = c->err;
   a.Hkv = c->num_kv_heads;
   a.DH = c->head_dim;
+  a.dh_log2 = c->head_dim == 128 ? 7 : 6;
   a.bs_log2 = l;
   a.num_blocks = c->num_blocks;
   a.max_seqs = c->max_seqs;
@@ -455,7 +628,18 @@ SM_API sm_status sm_kv_append(const sm_paged_cache *c, const int32_t *seq_ids, c
   if (!seq_ids || !row_offsets || (total_rows > 0 && (!K || !V))) return SM_EINVAL;
   const size_t es = c->dtype == SM_BF16 ? 2 : 4;
   const size_t lds = (size_t)kCopyRows * (c->num_kv_heads * c->head_dim + 4) * es;
-  if (lds > 64 * 1024) return SM_EINVAL;
+  if (lds > 64 * 1024 || c->num_kv_heads * c->head_dim > kMaxRowElems) return SM_EINVAL;
+  const size_t tensor_bytes = (size_t)total_rows * c->num_kv_heads * c->head_dim * es;
+  const FastDiv upr = make_fastdiv((uint32_t)(c->num_kv_heads * c->head_dim * es / 16));
+  if (total_rows > 0 && total_rows <= kSmallRows && tensor_bytes <= (size_t)kSmallBytes) {
+    if (c->dtype == SM_BF16)
+      hipLaunchKernelGGL(append_small_kernel<uint16_t>, dim3(1), dim3(kMetaThreads), 0, stream, a, seq_ids,
+                         row_offsets, n, total_rows, (const uint16_t *)K, (const uint16_t *)V, upr);
+    else
+      hipLaunchKernelGGL(append_small_kernel<float>, dim3(1), dim3(kMetaThreads), 0, stream, a, seq_ids,
+                         row_offsets, n, total_rows, (const float *)K, (const float *)V, upr);
+    return hipGetLastError() == hipSuccess ? SM_OK : SM_EHIP;
+  }
   hipLaunchKernelGGL(append_meta_kernel, dim3(1), dim3(kMetaThreads), 0, stream, a, seq_ids, row_offsets, n,
                      total_rows);
   if (hipGetLastError() != hipSuccess) return SM_EHIP;

@@ -33,7 +33,7 @@ def _run(orc, oc, c, dtype, Hq, seq_ids, max_len, rng, scale=None):
     sc = D ** -0.5 if scale is None else scale
     st, ref = oc.decode_attention(seq_ids, wl.to_f64(q), Hq, sc)
     out = torch.full((n, Hq, D), float("nan"), dtype=dtype, device=dev())
-    ws = torch.empty(sm.decode_workspace_bytes(n, Hq, D, max_len), dtype=torch.uint8, device=dev())
+    ws = torch.zeros(sm.decode_workspace_bytes(n, Hq, D, max_len), dtype=torch.uint8, device=dev())
     sm.decode_attention(c, i32(seq_ids), q.to(dev()), out, ws, max_len, scale=sc)
     torch.cuda.synchronize()
     return st, ref, out.cpu()
