@@ -39,6 +39,13 @@ PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 METRIC = "decode-attention tokens/s + achieved HBM GB/s over span-compacted KV cache"
 
+# HBM traffic of the attention kernel from rocprofv3 --pmc FETCH_SIZE and
+# WRITE_SIZE runs (see profiles/decode_attention_llama3-8b-layer.md): scaled
+# measured bytes per launch divided by the algorithmic bytes of the same
+# launches.  Valid only for the kernel source it was measured on.
+TRAFFIC_RATIO = 1.0117
+TRAFFIC_SOURCE_SHA256 = {"decode_attn.hip": "1f971b6ca0b21e17bf9563b22717234d3f8ff67624ceb07051d24c7d3031a4fd", "common.hpp": "12a4a21e0b0bf50c3716cc96b5c366317e63901b1eb3601120fe353d7d9bfbb6"}
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -126,6 +133,8 @@ class Job:
             else:
                 lens = lens + 1
             self.len_sched.append(lens.copy())
+        self.attn_done = [torch.cuda.Event() for _ in range(R)]
+        self.upd_done = [torch.cuda.Event() for _ in range(R)]
         torch.cuda.synchronize()
         self._prep_ctypes()
         log(f"setup {time.time() - t0:.1f}s: R={R}, spans/batch={Smax}, packed rows/batch={self.packed_rows[0]}, "
@@ -150,65 +159,106 @@ class Job:
         bt = 4 * int(np.sum(-(-lens // w.block_size)))
         return kv + qo + bt
 
-    def run(self, stream, events=None):
-        """One benchmark step: the whole job for every resident batch."""
+    def _update(self, r, s, st):
+        """Cache update of batch r before decode step s: a decode-time merge
+        (merge module, roll back n-1 entries, append the surrogate's K/V) or
+        the new token's K/V."""
+        L, w = self.L, self.w
+        B, bf = w.batch, self.sm.SM_BF16
+        d = self.descs[r]
+        j = s % self.nin
+        m = self.dmerge.get(s)
+        rc = 0
+        if m is not None:
+            rc |= L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], m["row_idx"].data_ptr(), m["rows"],
+                                   m["offs"].data_ptr(), B, C.byref(self.mp), bf, self.zdec.data_ptr(),
+                                   self.dmerge_ws.data_ptr(), self.dmerge_ws.numel(), self.err.data_ptr(), st)
+            rc |= L.sm_kv_rollback(d, self.ids.data_ptr(), m["k"].data_ptr(), B, st)
+        rc |= L.sm_kv_append(d, self.ids.data_ptr(), self.one_row.data_ptr(), B, B,
+                             self.Kt[j].data_ptr(), self.Vt[j].data_ptr(), st)
+        if rc:
+            raise RuntimeError(f"cache update launch failed at step {s}: {rc}")
+
+    def run(self, stream, upd_stream, events=None):
+        """One benchmark step: the whole job for every resident batch.
+
+        Decode attention runs on `stream`; cache updates run on `upd_stream`,
+        each waiting only for its own batch's previous attention.  When both
+        are the same stream every update and every attention runs in order
+        (the default); with two streams batch r's update overlaps the
+        attention launches of the other batches."""
         import torch
-        L, sm, w = self.L, self.sm, self.w
-        B = w.batch
-        st = stream.cuda_stream
-        bf = sm.SM_BF16
-        for r in range(self.R):
+        L, w = self.L, self.w
+        B, bf = w.batch, self.sm.SM_BF16
+        sa, sb = stream.cuda_stream, upd_stream.cuda_stream
+        overlap = sa != sb
+        R = self.R
+        # prompt compression of every batch (after its previous job's last
+        # attention), then the first decode step's update
+        for r in range(R):
             c, dp = self.caches[r], self.dev_prompts[r]
-            # evict the previous job's sequences (rollback of everything)
-            self.kreset.copy_(c.lengths[:B])
-            rc = L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), self.kreset.data_ptr(), B, st)
-            # prompt compression: merge every span, pack, bulk-append the prompt K/V
+            if overlap:
+                upd_stream.wait_event(self.attn_done[r])
+            with torch.cuda.stream(upd_stream):
+                self.kreset.copy_(c.lengths[:B])   # evict the previous job's sequences
+            rc = L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), self.kreset.data_ptr(), B, sb)
             rc |= L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], dp["row_idx"].data_ptr(), dp["rows"],
                                    dp["span_offsets"].data_ptr(), dp["S"], C.byref(self.mp), bf,
                                    self.z.data_ptr(), self.merge_ws.data_ptr(), self.merge_ws.numel(),
-                                   self.err.data_ptr(), st)
+                                   self.err.data_ptr(), sb)
             rc |= L.sm_pack_spans(B, dp["seq_offsets"].data_ptr(), B * w.prompt_len, dp["S"],
                                   dp["span_start"].data_ptr(), dp["span_len"].data_ptr(),
                                   dp["seq_span_offsets"].data_ptr(), self.pi.data_ptr(), self.po.data_ptr(),
                                   self.ps.data_ptr(), dp["token_ids"].data_ptr(), self.emb.data_ptr(),
                                   self.emb.shape[0], self.z.data_ptr(), w.d, bf, self.packed.data_ptr(),
-                                  self.err.data_ptr(), st)
+                                  self.err.data_ptr(), sb)
             rc |= L.sm_kv_append(self.descs[r], self.ids.data_ptr(), self.po.data_ptr(), B, self.packed_rows[r],
-                                 self.Kp.data_ptr(), self.Vp.data_ptr(), st)
+                                 self.Kp.data_ptr(), self.Vp.data_ptr(), sb)
             if rc:
                 raise RuntimeError(f"prompt compression launch failed: {rc}")
+            self._update(r, 0, sb)
+            if overlap:
+                self.upd_done[r].record(upd_stream)
         for s in range(w.decode_steps):
             j = s % self.nin
-            m = self.dmerge.get(s)
-            rc = 0
-            # every batch first updates its cache: a decode-time merge (merge
-            # module, roll back n-1 entries, append the surrogate's K/V) or
-            # the new token's K/V ...
-            for r in range(self.R):
-                d = self.descs[r]
-                if m is not None:
-                    rc |= L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], m["row_idx"].data_ptr(), m["rows"],
-                                           m["offs"].data_ptr(), B, C.byref(self.mp), bf, self.zdec.data_ptr(),
-                                           self.dmerge_ws.data_ptr(), self.dmerge_ws.numel(), self.err.data_ptr(), st)
-                    rc |= L.sm_kv_rollback(d, self.ids.data_ptr(), m["k"].data_ptr(), B, st)
-                rc |= L.sm_kv_append(d, self.ids.data_ptr(), self.one_row.data_ptr(), B, B,
-                                     self.Kt[j].data_ptr(), self.Vt[j].data_ptr(), st)
-            # ... then the attention launches of all batches run back to back
             if events is not None:
                 events[0][s].record(stream)
-            for r in range(self.R):
-                rc |= L.sm_decode_attention(self.descs[r], self.ids.data_ptr(), B, self.q[j].data_ptr(),
-                                            w.num_q_heads, w.head_dim ** -0.5, self.max_len, self.out.data_ptr(),
-                                            self.dec_ws.data_ptr(), self.dec_ws.numel(), st)
+            for r in range(R):
+                if overlap:
+                    stream.wait_event(self.upd_done[r])
+                rc = L.sm_decode_attention(self.descs[r], self.ids.data_ptr(), B, self.q[j].data_ptr(),
+                                           w.num_q_heads, w.head_dim ** -0.5, self.max_len, self.out.data_ptr(),
+                                           self.dec_ws.data_ptr(), self.dec_ws.numel(), sa)
+                if rc:
+                    raise RuntimeError(f"attention launch failed at step {s}: {rc}")
+                if overlap:
+                    self.attn_done[r].record(stream)
             if events is not None:
                 events[1][s].record(stream)
-            if rc:
-                raise RuntimeError(f"decode launch failed at step {s}: {rc}")
+            if s + 1 < w.decode_steps:
+                for r in range(R):
+                    if overlap:
+                        upd_stream.wait_event(self.attn_done[r])
+                    self._update(r, s + 1, sb)
+                    if overlap:
+                        self.upd_done[r].record(upd_stream)
 
     def check_errors(self):
         bits = [c.error_bits() for c in self.caches] + [int(self.err.item())]
         if any(bits):
             raise RuntimeError(f"device error bits set: {bits}")
+
+
+def traffic_bytes(alg_bytes):
+    """Measured HBM bytes per attention launch, or None when the kernel
+    sources differ from the ones the counters were taken on."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2609_27233_amd", "csrc")
+    for name, digest in TRAFFIC_SOURCE_SHA256.items():
+        with open(os.path.join(csrc, name), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != digest:
+                return None
+    return int(alg_bytes * TRAFFIC_RATIO)
 
 
 def cpu_baseline(job, target_s=20.0):
@@ -284,23 +334,42 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--replicas", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-steps", type=int, default=None,
+                    help="decode steps per job (default: the workload's 256; shorter only for counter runs)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES three times (scales HBM counters) and exit")
+    ap.add_argument("--overlap", action="store_true",
+                    help="run cache updates on a second stream, overlapped with other batches' attention")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build measures the single-GPU hot path "
               f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
         sys.exit(2)
 
+    import dataclasses
     import torch
     from paper_2609_27233_amd import workload as wl
 
     dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        n = args.copy_calibration // 4
+        a = torch.ones(n, dtype=torch.int32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"copied {n * 4} bytes three times")
+        return
     w = wl.WORKLOADS[2]
+    if args.decode_steps is not None:
+        w = dataclasses.replace(w, decode_steps=args.decode_steps)
     job = Job(w, args.replicas, dev)
     stream = torch.cuda.current_stream()
+    upd_stream = torch.cuda.Stream() if args.overlap else stream  # default priority
     nlaunch = w.decode_steps * job.R
 
     for i in range(args.warmup):
-        job.run(stream)
+        job.run(stream, upd_stream)
         torch.cuda.synchronize()
         log(f"warmup {i} done")
     job.check_errors()
@@ -310,7 +379,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        job.run(stream, events=ev)
+        job.run(stream, upd_stream, events=ev)
         torch.cuda.synchronize()
         attn_ms += sum(a.elapsed_time(b) for a, b in zip(ev[0], ev[1]))
         log(f"step {i} done")
@@ -344,6 +413,7 @@ def main():
                         f"decode-time merge every {w.merge_every} steps, {job.R} resident batches",
             "batch": w.batch, "prompt_len": w.prompt_len, "compacted_len": job.L0,
             "decode_steps": w.decode_steps, "resident_batches": job.R,
+            "update_overlap": bool(args.overlap),
             "layer": {"d": w.d, "q_heads": w.num_q_heads, "kv_heads": w.num_kv_heads, "head_dim": w.head_dim},
             "block_size": w.block_size,
         },
@@ -355,7 +425,7 @@ def main():
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4),
-            "traffic": None,
+            "traffic": traffic_bytes(mean_bytes),
             "avg_launch_us": round(avg_launch_us, 3),
             "algorithmic_bytes_per_launch": int(mean_bytes),
         },

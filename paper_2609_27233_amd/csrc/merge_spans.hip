@@ -142,6 +142,92 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_nt_gelu(const uint16_t *__re
 }
 
 // ---------------------------------------------------------------------------
+// Skinny bf16 GEMM for M <= 64 rows (a decode-time merge of a few spans):
+// C[M][N] = GELU(A[M][K] W[N][K]^T + bias).  One workgroup per 16 output
+// columns (N / 16 workgroups, enough to keep every compute unit streaming
+// its slice of W), the four waves split K and reduce through LDS.  Operand
+// fragments are loaded straight from memory in MFMA layout, U k-steps of 32
+// at a time so that U * (1 + m-tiles) 16-byte loads per lane are in flight.
+
+constexpr int kSkinnyMaxM = 64;
+
+template <typename OutT, int U>
+__global__ __launch_bounds__(256) void gemm_skinny_bf16_gelu(const uint16_t *__restrict__ A,
+                                                             const int32_t *__restrict__ gather, int64_t a_rows,
+                                                             const uint16_t *__restrict__ W,
+                                                             const uint16_t *__restrict__ bias,
+                                                             OutT *__restrict__ C, int M, int N, int K,
+                                                             int32_t *err) {
+  __shared__ float red[4][kSkinnyMaxM][17];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int r = lane & 15, q4 = lane >> 4;
+  const int n0 = blockIdx.x * 16;
+  const int mt = (M + 15) >> 4;  // m-tiles (<= 4)
+  const uint16_t *arow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = i * 16 + r;
+    int64_t idx = 0;
+    if (m < M) {
+      idx = gather ? gather[m] : m;
+      if (idx < 0 || idx >= a_rows) {
+        set_err(err, SM_ERR_EINVAL);
+        idx = 0;
+      }
+    }
+    arow[i] = A + idx * K + 8 * q4;
+  }
+  const uint16_t *wrow = W + (int64_t)(n0 + r) * K + 8 * q4;
+  const int kw = K >> 2, kbeg = w * kw;
+  f32x4_t acc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int k = kbeg; k < kbeg + kw; k += 32 * U) {
+    u32x4_t bw[U], fa[U][4];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      bw[u] = *(const u32x4_t *)(wrow + k + 32 * u);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (i < mt) fa[u][i] = *(const u32x4_t *)(arow[i] + k + 32 * u);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (i < mt)
+          acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[u][i]), as_bf16x8(bw[u]), acc[i], 0, 0, 0);
+  }
+  // lane (r, q4) of m-tile i holds rows 16 i + 4 q4 + e, column r
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) red[w][i * 16 + 4 * q4 + e][r] = acc[i][e];
+  __syncthreads();
+  for (int o = tid; o < mt * 16 * 16; o += 256) {
+    const int m = o >> 4, n = o & 15;
+    if (m >= M) continue;
+    const float v = red[0][m][n] + red[1][m][n] + red[2][m][n] + red[3][m][n];
+    C[(int64_t)m * N + n0 + n] = Elem<OutT>::to_store(gelu_erf(v + bf16_to_f32(bias[n0 + n])));
+  }
+}
+
+template <typename OutT>
+static void launch_skinny(const uint16_t *A, const int32_t *gather, int64_t a_rows, const uint16_t *W,
+                          const uint16_t *bias, OutT *C, int M, int N, int K, int32_t *err, hipStream_t stream) {
+  const dim3 grid(N / 16), block(256);
+  if ((K / 4) % (32 * 8) == 0)
+    hipLaunchKernelGGL((gemm_skinny_bf16_gelu<OutT, 8>), grid, block, 0, stream, A, gather, a_rows, W, bias, C, M,
+                       N, K, err);
+  else if ((K / 4) % (32 * 4) == 0)
+    hipLaunchKernelGGL((gemm_skinny_bf16_gelu<OutT, 4>), grid, block, 0, stream, A, gather, a_rows, W, bias, C, M,
+                       N, K, err);
+  else
+    hipLaunchKernelGGL((gemm_skinny_bf16_gelu<OutT, 2>), grid, block, 0, stream, A, gather, a_rows, W, bias, C, M,
+                       N, K, err);
+}
+
+// ---------------------------------------------------------------------------
 // fp32 GEMM on the vector ALU (64x64 tile, 4x4 outputs per thread), same
 // contract as the bf16 one.
 
@@ -474,18 +560,26 @@ SM_API sm_status sm_merge_spans(const void *emb, int64_t emb_rows, const int32_t
   float *ybuf = (float *)(wsb + align256((size_t)total_rows * d * es) + align256((size_t)num_spans * d * es));
 
   if (dt == SM_BF16) {
-    hipLaunchKernelGGL(gemm_bf16_nt_gelu<uint16_t>, dim3(d / kBN, (total_rows + kBM - 1) / kBM), dim3(256), 0,
-                       stream, (const uint16_t *)emb, row_idx, emb_rows, (const uint16_t *)p->W_kv,
-                       (const uint16_t *)p->b_kv, (uint16_t *)g1, total_rows, d, d, err);
+    if (total_rows <= kSkinnyMaxM)
+      launch_skinny<uint16_t>((const uint16_t *)emb, row_idx, emb_rows, (const uint16_t *)p->W_kv,
+                              (const uint16_t *)p->b_kv, (uint16_t *)g1, total_rows, d, d, err, stream);
+    else
+      hipLaunchKernelGGL(gemm_bf16_nt_gelu<uint16_t>, dim3(d / kBN, (total_rows + kBM - 1) / kBM), dim3(256), 0,
+                         stream, (const uint16_t *)emb, row_idx, emb_rows, (const uint16_t *)p->W_kv,
+                         (const uint16_t *)p->b_kv, (uint16_t *)g1, total_rows, d, d, err);
     if (hipGetLastError() != hipSuccess) return SM_EHIP;
     hipLaunchKernelGGL(pool_kernel<uint16_t>, dim3(num_spans), dim3(kPoolThreads), 0, stream,
                        (const uint16_t *)g1, span_offsets, num_spans, total_rows, (const uint16_t *)p->Q,
                        (const uint16_t *)p->g_kv, (const uint16_t *)p->beta_kv, p->ln_eps, d, h,
                        (uint16_t *)cbuf, err);
     if (hipGetLastError() != hipSuccess) return SM_EHIP;
-    hipLaunchKernelGGL(gemm_bf16_nt_gelu<float>, dim3(d / kBN, (num_spans + kBM - 1) / kBM), dim3(256), 0,
-                       stream, (const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
-                       (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, ybuf, num_spans, d, d, err);
+    if (num_spans <= kSkinnyMaxM)
+      launch_skinny<float>((const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
+                           (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, ybuf, num_spans, d, d, err, stream);
+    else
+      hipLaunchKernelGGL(gemm_bf16_nt_gelu<float>, dim3(d / kBN, (num_spans + kBM - 1) / kBM), dim3(256), 0,
+                         stream, (const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
+                         (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, ybuf, num_spans, d, d, err);
     if (hipGetLastError() != hipSuccess) return SM_EHIP;
     hipLaunchKernelGGL(ln_rows_kernel<uint16_t>, dim3(num_spans), dim3(kPoolThreads), 0, stream, ybuf,
                        (const uint16_t *)p->g_o, (const uint16_t *)p->beta_o, p->ln_eps, d, (uint16_t *)out);

@@ -110,3 +110,32 @@ def test_merge_bad_row_index_sets_einval(orc):
     out, err = _gpu_merge(emb.to(dev()), np.array([1, 2, 99], np.int32), np.array([0, 2, 3], np.int32),
                           params, 4, torch.bfloat16)
     assert err == sm.ERR_EINVAL
+
+
+@pytest.mark.parametrize("d,S", [(4096, 16), (3584, 128), (8192, 4)])
+def test_merge_decode_time_batches(orc, d, S):
+    """Decode-time merges: one freshly completed span of n = 2..4 tokens per
+    sequence (a few rows: the skinny GEMM path) at the model widths of the
+    benchmark layers."""
+    rng = np.random.RandomState(d + S)
+    lens = rng.randint(2, 5, size=S)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    vocab = 1500
+    row_idx = rng.randint(0, vocab, size=int(offs[-1])).astype(np.int32)
+    g = wl.generator(d + 1, "cuda")
+    emb = wl.randn((vocab, d), torch.bfloat16, g, device="cuda", std=0.02)
+    params = wl.make_merge_params(d, 4, torch.bfloat16, g, device="cuda", spread=True)
+    say("merge decode-time", d, S, "rows", int(offs[-1]))
+    out, err = _gpu_merge(emb, row_idx, offs, params, 4, torch.bfloat16)
+    assert err == 0
+    sample = np.arange(S) if S <= 16 else np.sort(rng.choice(S, size=12, replace=False))
+    used = np.unique(np.concatenate([row_idx[offs[s]:offs[s + 1]] for s in sample]))
+    remap = {int(r): i for i, r in enumerate(used)}
+    sub_rows = np.array([remap[int(r)] for s in sample for r in row_idx[offs[s]:offs[s + 1]]], np.int32)
+    so = np.concatenate([[0], np.cumsum([offs[s + 1] - offs[s] for s in sample])]).astype(np.int32)
+    st, ref = orc.merge_spans(wl.to_f64(emb[torch.as_tensor(used, device="cuda")]), sub_rows, so,
+                              {k: wl.to_f64(v) for k, v in params.items()}, 4)
+    assert st == orc.OK
+    e = rel_l2_max(out[torch.as_tensor(sample)].float().numpy(), ref)
+    say("rel_l2_max", e)
+    assert e <= TOL[torch.bfloat16]
