@@ -249,6 +249,165 @@ class Job:
             raise RuntimeError(f"device error bits set: {bits}")
 
 
+def _time(fn, stream, reps):
+    """Average ms of fn() over reps calls, HIP events on `stream`."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def extras_report(job, stream, attn_us):
+    """Side measurements named in the workload description: the same
+    attention over the uncompressed cache (control), the merge module at the
+    70B-shaped prompt batch (MFMA utilisation), and the cache operations."""
+    import torch
+    from paper_2609_27233_amd import workload as wl
+    sm, L, w, dev = job.sm, job.L, job.w, job.dev
+    B, H, D, Hq, bs = w.batch, w.num_kv_heads, w.head_dim, w.num_q_heads, w.block_size
+    st = stream.cuda_stream
+    out = {}
+    g = wl.generator(77, dev)
+    ids = job.ids
+
+    # --- uncompressed control: same launch shape, cache length = prompt + 128
+    Lu = w.prompt_len + 128
+    nb = -(-Lu // bs) + 1
+    caches = []
+    Ku = wl.randn((B * Lu, H, D), w.torch_dtype, g, device=dev)
+    Vu = wl.randn((B * Lu, H, D), w.torch_dtype, g, device=dev)
+    offs = torch.as_tensor(np.arange(B + 1, dtype=np.int32) * Lu).to(dev)
+    for r in range(job.R):
+        c = sm.PagedCache(dtype=w.torch_dtype, num_kv_heads=H, head_dim=D, block_size=bs, num_blocks=B * nb,
+                          max_seqs=B, max_blocks_per_seq=nb, device=dev)
+        sm.kv_append(c, ids, offs, Ku, Vu, stream=stream)
+        caches.append(c)
+    del Ku, Vu
+    ws = torch.zeros(sm.decode_workspace_bytes(B, Hq, D, Lu), dtype=torch.uint8, device=dev)
+    descs = [C.byref(c.desc) for c in caches]
+
+    def attn_all():
+        for d in descs:
+            L.sm_decode_attention(d, ids.data_ptr(), B, job.q[0].data_ptr(), Hq, D ** -0.5, Lu,
+                                  job.out.data_ptr(), ws.data_ptr(), ws.numel(), st)
+    ms = _time(attn_all, stream, 16) / job.R
+    ubytes = job.decode_bytes(np.full(B, Lu))
+    out["uncompressed_control"] = {
+        "cache_len": Lu, "avg_launch_us": round(ms * 1e3, 3),
+        "achieved_GBps": round(ubytes / (ms * 1e-3) / 1e9, 1),
+        "compacted_avg_launch_us": round(attn_us, 3),
+        "speedup_per_step": round(ms * 1e3 / attn_us, 3),
+        "note": "per decode step of the same batch: uncompressed cache (prompt 4096 + 128) vs span-compacted "
+                "cache (mean over the job's 256 steps)"}
+    assert all(c.error_bits() == 0 for c in caches)
+    log("extras: uncompressed control done")
+    del caches, descs, ws
+    torch.cuda.empty_cache()
+
+    # --- cache operations on a fresh cache of the job's shape
+    c = sm.PagedCache(dtype=w.torch_dtype, num_kv_heads=H, head_dim=D, block_size=bs,
+                      num_blocks=job.caches[0].num_blocks, max_seqs=B,
+                      max_blocks_per_seq=job.caches[0].max_blocks, device=dev)
+    d = C.byref(c.desc)
+    rows = job.packed_rows[0]
+    kfull = torch.full((B,), job.L0, dtype=torch.int32, device=dev)
+
+    def bulk():
+        L.sm_kv_append(d, ids.data_ptr(), job.po.data_ptr(), B, rows, job.Kp.data_ptr(), job.Vp.data_ptr(), st)
+        L.sm_kv_rollback(d, ids.data_ptr(), kfull.data_ptr(), B, st)
+    # packed offsets of batch 0 for the bulk append
+    po = np.concatenate([[0], np.cumsum(np.full(B, job.L0))]).astype(np.int32)
+    job.po.copy_(torch.as_tensor(po))
+    t_bulk_roll = _time(bulk, stream, 5)
+    L.sm_kv_append(d, ids.data_ptr(), job.po.data_ptr(), B, rows, job.Kp.data_ptr(), job.Vp.data_ptr(), st)
+    def step_append():
+        L.sm_kv_append(d, ids.data_ptr(), job.one_row.data_ptr(), B, B, job.Kt[0].data_ptr(),
+                       job.Vt[0].data_ptr(), st)
+    t_app = _time(step_append, stream, 100)          # 101 appends: L0 + 101 entries per sequence
+    k1 = torch.ones(B, dtype=torch.int32, device=dev)
+    k3 = torch.full((B,), 3, dtype=torch.int32, device=dev)
+    t_roll = _time(lambda: L.sm_kv_rollback(d, ids.data_ptr(), k1.data_ptr(), B, st), stream, 40)
+
+    def merge_update():                              # one decode-time merge of n = 4: crop 3, append 1
+        L.sm_kv_rollback(d, ids.data_ptr(), k3.data_ptr(), B, st)
+        L.sm_kv_append(d, ids.data_ptr(), job.one_row.data_ptr(), B, B, job.Kt[1].data_ptr(),
+                       job.Vt[1].data_ptr(), st)
+    t_mu = _time(merge_update, stream, 20)
+    dp = job.dev_prompts[0]
+
+    def pack():
+        L.sm_pack_spans(B, dp["seq_offsets"].data_ptr(), B * w.prompt_len, dp["S"], dp["span_start"].data_ptr(),
+                        dp["span_len"].data_ptr(), dp["seq_span_offsets"].data_ptr(), job.pi.data_ptr(),
+                        job.po.data_ptr(), job.ps.data_ptr(), dp["token_ids"].data_ptr(), job.emb.data_ptr(),
+                        job.emb.shape[0], job.z.data_ptr(), w.d, sm.SM_BF16, job.packed.data_ptr(),
+                        job.err.data_ptr(), st)
+    t_pack = _time(pack, stream, 5)
+    assert c.error_bits() == 0 and int(job.err.item()) == 0
+    row_bytes = H * D * 2
+    out["cache_ops"] = {
+        "bulk_append_rows": rows,
+        "bulk_append_plus_full_rollback_ms": round(t_bulk_roll, 4),
+        "bulk_append_GBps": round(4 * rows * row_bytes / (t_bulk_roll * 1e-3) / 1e9, 1),
+        "decode_append_16_rows_us": round(t_app * 1e3, 2),
+        "rollback_16_seqs_k1_us": round(t_roll * 1e3, 2),
+        "merge_update_16_seqs_us": round(t_mu * 1e3, 2),
+        "pack_prompt_batch_us": round(t_pack * 1e3, 1),
+        "pack_GBps": round((2 * rows * w.d * 2 + 8 * B * w.prompt_len) / (t_pack * 1e-3) / 1e9, 1),
+        "note": "HIP events around back-to-back calls on one stream; merge update = roll back 3 entries and "
+                "append the surrogate's K/V for each of 16 sequences; "
+                "bytes: append reads and writes K and V, pack reads and writes the packed rows plus indices"}
+    log("extras: cache operations done")
+    del c
+    torch.cuda.empty_cache()
+
+    out["merge_spans_70b_prompt_batch"] = merge_70b_report(job.sm, job.L, dev, stream)
+    return out
+
+
+def merge_70b_report(sm, L, dev, stream, reps=3):
+    """The merge module over every span of the 32 x 8192 Llama-3-70B-shaped
+    prompt batch in one call: time and MFMA utilisation."""
+    import torch
+    from paper_2609_27233_amd import workload as wl
+    st = stream.cuda_stream
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    w5 = wl.WORKLOADS[5]
+    P5 = wl.make_prompts(w5)
+    g5 = wl.generator(w5.seed, dev)
+    emb5 = wl.randn((w5.vocab, w5.d), torch.bfloat16, g5, device=dev, std=0.02)
+    par5 = wl.make_merge_params(w5.d, w5.h, torch.bfloat16, g5, device=dev)
+    S5, R5 = len(P5.span_len), len(P5.row_idx)
+    i32 = lambda a: torch.as_tensor(np.asarray(a, np.int32)).to(dev)
+    ri, so = i32(P5.row_idx), i32(P5.span_offsets)
+    z5 = torch.empty((S5, w5.d), dtype=torch.bfloat16, device=dev)
+    ws5 = torch.empty(sm.merge_workspace_bytes(R5, S5, w5.d, torch.bfloat16), dtype=torch.uint8, device=dev)
+    mp5 = sm.MergeParams(w5.d, w5.h, 1e-5, *(par5[k].data_ptr() for k in
+                         ("Q", "W_kv", "b_kv", "g_kv", "beta_kv", "W_o", "b_o", "g_o", "beta_o")))
+
+    def merge5():
+        rc = L.sm_merge_spans(emb5.data_ptr(), emb5.shape[0], ri.data_ptr(), R5, so.data_ptr(), S5, C.byref(mp5),
+                              sm.SM_BF16, z5.data_ptr(), ws5.data_ptr(), ws5.numel(), err.data_ptr(), st)
+        if rc:
+            raise RuntimeError(f"sm_merge_spans failed: {rc}")
+    torch.cuda.synchronize()
+    log(f"extras: merge module inputs ready ({S5} spans, {R5} rows)")
+    t5 = _time(merge5, stream, reps)
+    flop5 = 2.0 * w5.d * w5.d * (R5 + S5)
+    assert int(err.item()) == 0
+    return {
+        "spans": S5, "rows": R5, "d": w5.d, "ms": round(t5, 3),
+        "TFLOPs": round(flop5 / (t5 * 1e-3) / 1e12, 1),
+        "frac_of_bf16_peak": round(flop5 / (t5 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "note": "one sm_merge_spans call over every span of the 32 x 8192 prompts; FLOP = 2 d^2 (rows + spans) "
+                "for the two projections (pooling and LayerNorm are O(d) per row)"}
+
+
 def traffic_bytes(alg_bytes):
     """Measured HBM bytes per attention launch, or None when the kernel
     sources differ from the ones the counters were taken on."""
@@ -334,10 +493,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--replicas", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true", help="skip the side measurements")
     ap.add_argument("--decode-steps", type=int, default=None,
                     help="decode steps per job (default: the workload's 256; shorter only for counter runs)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES three times (scales HBM counters) and exit")
+    ap.add_argument("--merge-only", action="store_true",
+                    help="only time the merge module over the 70B-shaped prompt batch and print that")
     ap.add_argument("--overlap", action="store_true",
                     help="run cache updates on a second stream, overlapped with other batches' attention")
     args = ap.parse_args()
@@ -359,6 +521,10 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         log(f"copied {n * 4} bytes three times")
+        return
+    if args.merge_only:
+        from paper_2609_27233_amd import lib as sm
+        print(json.dumps(merge_70b_report(sm, sm.load(), dev, torch.cuda.current_stream(), reps=5)), flush=True)
         return
     w = wl.WORKLOADS[2]
     if args.decode_steps is not None:
@@ -430,6 +596,12 @@ def main():
             "algorithmic_bytes_per_launch": int(mean_bytes),
         },
     }
+    if not args.no_extras and args.decode_steps is None:
+        try:
+            result["extras"] = extras_report(job, stream, avg_launch_us)
+        except Exception as e:          # side measurements never hide the main line
+            log(f"extras failed: {e!r}")
+            result["extras"] = {"error": repr(e)}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(job)
     print(json.dumps(result), flush=True)
