@@ -16,6 +16,8 @@
 // The fp32 dtype runs the same four steps with a vector-ALU GEMM.
 #include "common.hpp"
 
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
 namespace sm {
 
 // ---------------------------------------------------------------------------
@@ -139,6 +141,237 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_nt_gelu(const uint16_t *__re
       }
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Large bf16 GEMM, same contract as above: 256x256 output tile per
+// workgroup, eight waves in a 2 x 4 grid (128 x 64 each) on
+// v_mfma_f32_32x32x16_bf16 (the 32x32 form sustains the full matrix-core
+// rate on gfx950; the 16x16x32 form measured about 64% of it).  K advances
+// 32 at a time through a ring of four LDS stages (4 x 32 KB) filled by
+// global_load_lds_dwordx4, which moves 16 bytes per lane from memory
+// straight into LDS without staging registers.  Waits are explicit
+// (s_waitcnt vmcnt + s_barrier) so that two k-tiles stay in flight behind
+// the one being consumed; each wave reads its next fragments while its
+// matrix cores work on the current ones, and the scheduler interleaves the
+// LDS reads and the ring refills with the MFMAs.
+//
+// LDS layout of one operand stage: 256 rows x 64 bytes as 16-byte slots
+// row * 4 + (chunk ^ ((row >> 1) & 3)); the swizzle keeps the fragment
+// reads free of bank conflicts.  A direct-to-LDS load writes 64
+// consecutive slots (one per lane), so lane l of a load covers row
+// base + l / 4, slot chunk l % 4, and fetches global chunk
+// (l % 4) ^ swizzle(row).
+//
+// Tile order: the hardware hands workgroup b to XCD b % 8; XCD x takes the
+// logical tiles [x * per_xcd, (x + 1) * per_xcd) in groups of kGroupM row
+// tiles, so the 32 tiles in flight on one XCD share A rows and B columns
+// in its L2.
+
+constexpr int kLM = 256, kLN = 256, kLK = 32, kLStages = 4, kLThreads = 512, kGroupM = 4;
+constexpr int kLStageBytes = kLM * kLK * 2;  // per operand
+constexpr int kLLdsBytes = 2 * kLStages * kLStageBytes;
+
+__device__ __forceinline__ int lds_swz(int row) { return (row >> 1) & 3; }
+
+// s_waitcnt with vmcnt = N, lgkmcnt = 0, expcnt left open
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
+__device__ __forceinline__ void load_to_lds16(const uint16_t *src, uint8_t *lds) {
+  __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1))) *)src,
+                                   (void __attribute__((address_space(3))) *)lds, 16, 0, 0);
+}
+
+template <typename OutT>
+struct Store4;
+template <>
+struct Store4<float> {
+  static __device__ __forceinline__ void put(float *p, float a, float b, float c, float d) {
+    *(f32x4_t *)p = f32x4_t{a, b, c, d};
+  }
+};
+template <>
+struct Store4<uint16_t> {
+  static __device__ __forceinline__ void put(uint16_t *p, float a, float b, float c, float d) {
+    *(uint2 *)p = make_uint2(pack_bf16x2(a, b), pack_bf16x2(c, d));
+  }
+};
+
+template <typename OutT>
+__global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
+    const uint16_t *__restrict__ A, const int32_t *__restrict__ gather, int64_t a_rows,
+    const uint16_t *__restrict__ B, const uint16_t *__restrict__ bias, OutT *__restrict__ C, int M, int N, int K,
+    int tiles_m, int tiles_n, int per_xcd, int32_t *err) {
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w >> 2, wn = w & 3;  // this wave's 128 x 64 block of the tile
+  const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (t >= tiles_m * tiles_n) return;
+  const int gsz = kGroupM * tiles_n;
+  const int g0 = (t / gsz) * kGroupM;
+  const int gm = min(kGroupM, tiles_m - g0);
+  const int tm = g0 + (t % gsz) % gm, tn = (t % gsz) / gm;
+  const int m0 = tm * kLM, n0 = tn * kLN;
+
+  // sources of this lane's two loads per operand and stage (rows
+  // (u * 8 + w) * 16 + lane / 4); A rows past M re-read a valid row
+  const uint16_t *pa[2], *pb[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int row = (u * 8 + w) * 16 + (lane >> 2);
+    const int chunk = (lane & 3) ^ lds_swz(row);
+    int64_t arow = m0 + row;
+    if (gather) {
+      int gi = (arow < M) ? gather[arow] : 0;
+      if (gi < 0 || gi >= a_rows) {
+        set_err(err, SM_ERR_EINVAL);
+        gi = 0;
+      }
+      arow = gi;
+    } else if (arow >= M) {
+      arow = M - 1;
+    }
+    pa[u] = A + arow * K + chunk * 8;
+    pb[u] = B + (int64_t)(n0 + row) * K + chunk * 8;
+  }
+  uint8_t *sa = lds, *sb = lds + kLStages * kLStageBytes;
+  auto refill = [&](int kt, int stage) {  // k-tile kt into ring stage `stage`
+    const int ko = kt * kLK;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      load_to_lds16(pa[u] + ko, sa + stage * kLStageBytes + (u * 8 + w) * 1024);
+      load_to_lds16(pb[u] + ko, sb + stage * kLStageBytes + (u * 8 + w) * 1024);
+    }
+  };
+
+  // 32x32x16 operands: lane l feeds row l % 32, k 8 (l / 32) .. +7 of a
+  // 16-wide k step, i.e. chunk 2 ks + l / 32 of the 64-byte row
+  const int r32 = lane & 31, h2 = lane >> 5;
+  const int fo0 = (r32 * 4 + (h2 ^ lds_swz(r32))) * 16;
+  const int fo1 = (r32 * 4 + ((2 + h2) ^ lds_swz(r32))) * 16;
+  const int a_off = wm * 128 * 64, b_off = wn * 64 * 64;
+
+  f32x16_t acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // fa[4 ks + i]: rows 32 i of k step ks; fb[2 ks + j]: columns 32 j
+#define SM_READ_FRAGS(KT, FA, FB)                                                          \
+  {                                                                                        \
+    const uint8_t *la_ = sa + ((KT) & (kLStages - 1)) * kLStageBytes + a_off;              \
+    const uint8_t *lb_ = sb + ((KT) & (kLStages - 1)) * kLStageBytes + b_off;              \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                        \
+      FA[i] = *(const u32x4_t *)(la_ + i * 2048 + fo0);                                    \
+      FA[4 + i] = *(const u32x4_t *)(la_ + i * 2048 + fo1);                                \
+    }                                                                                      \
+    _Pragma("unroll") for (int j = 0; j < 2; ++j) {                                        \
+      FB[j] = *(const u32x4_t *)(lb_ + j * 2048 + fo0);                                    \
+      FB[2 + j] = *(const u32x4_t *)(lb_ + j * 2048 + fo1);                                \
+    }                                                                                      \
+  }
+  // swapped operands: the MFMA computes D[n][m], so a lane ends up holding
+  // four consecutive output columns of one row
+#define SM_MMA(FA, FB)                                                                     \
+  _Pragma("unroll") for (int ks = 0; ks < 2; ++ks)                                         \
+  _Pragma("unroll") for (int i = 0; i < 4; ++i)                                            \
+  _Pragma("unroll") for (int j = 0; j < 2; ++j)                                            \
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(FB[2 * ks + j]),         \
+                                                        as_bf16x8(FA[4 * ks + i]), acc[i][j], 0, 0, 0);
+  // 16 MFMAs, 12 fragment reads and 4 ring loads per wave and k-tile
+#define SM_INTERLEAVE()                                                                    \
+  {                                                                                        \
+    _Pragma("unroll") for (int g = 0; g < 12; ++g) {                                       \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                   \
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                                   \
+      if (g < 4) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                        \
+    }                                                                                      \
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                     \
+  }
+
+  // Ring: k-tile t lives in stage t % 4.  The step that multiplies k-tile kt
+  // waits for kt + 1, passes the barrier (after which no wave still reads
+  // the stage of kt), refills that stage with k-tile kt + 4 and reads the
+  // fragments of kt + 1.  Past the end the last k-tile is loaded again
+  // (never read) so that the in-flight count, and thus every wait, is the
+  // same at each step.  Requires K % 64 == 0 and K >= 256.
+  const int nk = K / kLK;
+#pragma unroll
+  for (int st = 0; st < kLStages; ++st) refill(st, st);
+  u32x4_t f0a[8], f0b[4], f1a[8], f1b[4];
+  wait_vmcnt_lgkm0<4 * (kLStages - 1)>();
+  __builtin_amdgcn_s_barrier();
+  SM_READ_FRAGS(0, f0a, f0b);
+  for (int kt = 0; kt < nk; kt += 2) {
+    wait_vmcnt_lgkm0<4 * (kLStages - 2)>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    refill(min(kt + kLStages, nk - 1), kt & (kLStages - 1));
+    SM_READ_FRAGS(kt + 1, f1a, f1b);
+    SM_MMA(f0a, f0b);
+    SM_INTERLEAVE();
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt_lgkm0<4 * (kLStages - 2)>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    refill(min(kt + 1 + kLStages, nk - 1), (kt + 1) & (kLStages - 1));
+    SM_READ_FRAGS(kt + 2, f0a, f0b);  // past the end: reads a stale stage, unused
+    SM_MMA(f1a, f1b);
+    SM_INTERLEAVE();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  wait_vmcnt_lgkm0<0>();
+#undef SM_READ_FRAGS
+#undef SM_MMA
+#undef SM_INTERLEAVE
+
+  // 32x32 result layout (swapped): register 4 g + e of tile (i, j) holds
+  // C[row 32 i + r32][col 32 j + 8 g + 4 h2 + e]
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int col = n0 + wn * 64 + j * 32 + 8 * g + 4 * h2;
+      const uint2 bb = *(const uint2 *)(bias + col);
+      const float b0 = __uint_as_float(bb.x << 16), b1 = __uint_as_float(bb.x & 0xffff0000u);
+      const float b2 = __uint_as_float(bb.y << 16), b3 = __uint_as_float(bb.y & 0xffff0000u);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = m0 + wm * 128 + i * 32 + r32;
+        if (row < M)
+          Store4<OutT>::put(C + (int64_t)row * N + col, gelu_erf(acc[i][j][4 * g + 0] + b0),
+                            gelu_erf(acc[i][j][4 * g + 1] + b1), gelu_erf(acc[i][j][4 * g + 2] + b2),
+                            gelu_erf(acc[i][j][4 * g + 3] + b3));
+      }
+    }
+  }
+}
+
+static bool use_gemm256(int M, int N, int K) {
+  return N % kLN == 0 && K % (2 * kLK) == 0 && K >= 2 * kLK * kLStages &&
+         (int64_t)((M + kLM - 1) / kLM) * (N / kLN) >= 256;
+}
+
+template <typename OutT>
+static hipError_t launch_gemm256(const uint16_t *A, const int32_t *gather, int64_t a_rows, const uint16_t *B,
+                                 const uint16_t *bias, OutT *C, int M, int N, int K, int32_t *err,
+                                 hipStream_t stream) {
+  // dynamic LDS above 64 KB has to be enabled for the kernel (cheap; done
+  // on every launch so that it holds on whichever device is current)
+  const hipError_t e = hipFuncSetAttribute((const void *)gemm256_bf16_nt_gelu<OutT>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, kLLdsBytes);
+  if (e != hipSuccess) return e;
+  const int tiles_m = (M + kLM - 1) / kLM, tiles_n = N / kLN;
+  const int per_xcd = (tiles_m * tiles_n + 7) / 8;
+  hipLaunchKernelGGL(gemm256_bf16_nt_gelu<OutT>, dim3(8 * per_xcd), dim3(kLThreads), kLLdsBytes, stream, A, gather,
+                     a_rows, B, bias, C, M, N, K, tiles_m, tiles_n, per_xcd, err);
+  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -563,7 +796,12 @@ SM_API sm_status sm_merge_spans(const void *emb, int64_t emb_rows, const int32_t
     if (total_rows <= kSkinnyMaxM)
       launch_skinny<uint16_t>((const uint16_t *)emb, row_idx, emb_rows, (const uint16_t *)p->W_kv,
                               (const uint16_t *)p->b_kv, (uint16_t *)g1, total_rows, d, d, err, stream);
-    else
+    else if (use_gemm256(total_rows, d, d)) {
+      if (launch_gemm256<uint16_t>((const uint16_t *)emb, row_idx, emb_rows, (const uint16_t *)p->W_kv,
+                                   (const uint16_t *)p->b_kv, (uint16_t *)g1, total_rows, d, d, err,
+                                   stream) != hipSuccess)
+        return SM_EHIP;
+    } else
       hipLaunchKernelGGL(gemm_bf16_nt_gelu<uint16_t>, dim3(d / kBN, (total_rows + kBM - 1) / kBM), dim3(256), 0,
                          stream, (const uint16_t *)emb, row_idx, emb_rows, (const uint16_t *)p->W_kv,
                          (const uint16_t *)p->b_kv, (uint16_t *)g1, total_rows, d, d, err);
@@ -576,7 +814,12 @@ SM_API sm_status sm_merge_spans(const void *emb, int64_t emb_rows, const int32_t
     if (num_spans <= kSkinnyMaxM)
       launch_skinny<float>((const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
                            (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, ybuf, num_spans, d, d, err, stream);
-    else
+    else if (use_gemm256(num_spans, d, d)) {
+      if (launch_gemm256<float>((const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
+                                (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, ybuf, num_spans, d, d, err,
+                                stream) != hipSuccess)
+        return SM_EHIP;
+    } else
       hipLaunchKernelGGL(gemm_bf16_nt_gelu<float>, dim3(d / kBN, (num_spans + kBM - 1) / kBM), dim3(256), 0,
                          stream, (const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
                          (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, ybuf, num_spans, d, d, err);

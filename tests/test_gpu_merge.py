@@ -71,6 +71,32 @@ def test_merge_bf16_small(orc, d, S, nmax, spread):
     assert e <= TOL[torch.bfloat16]
 
 
+def test_merge_bf16_large_tiles(orc):
+    """Enough rows and spans that both projections take the 256 x 256-tile
+    GEMM (at least 256 output tiles), with ragged last row tiles; the oracle
+    checks a sample of spans from every part of the batch, the last ones
+    included."""
+    d, S = 512, 33000
+    rng = np.random.RandomState(77)
+    lens = rng.randint(1, 4, size=S)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    vocab = 5000
+    row_idx = rng.randint(0, vocab, size=int(offs[-1])).astype(np.int32)
+    assert (int(offs[-1]) + 255) // 256 * (d // 256) >= 256 and (S + 255) // 256 * (d // 256) >= 256
+    assert int(offs[-1]) % 256 and S % 256
+    g = wl.generator(d + 1)
+    emb = wl.randn((vocab, d), torch.bfloat16, g, std=0.02)
+    params = wl.make_merge_params(d, 4, torch.bfloat16, g, spread=True)
+    say("merge bf16 large tiles", d, S, "rows", int(offs[-1]))
+    out, err = _gpu_merge(emb.to(dev()), row_idx, offs, params, 4, torch.bfloat16)
+    assert err == 0
+    sample = np.unique(np.concatenate([rng.choice(S, 400, replace=False), np.arange(S - 300, S)]))
+    ref = _oracle(orc, wl.to_f64(emb), row_idx, offs, params, 4, sample=sample)
+    e = rel_l2_max(out.float().numpy()[sample], ref)
+    say("rel_l2_max", e)
+    assert e <= TOL[torch.bfloat16]
+
+
 def test_merge_llama3_8b_prompt_batch(orc):
     """All ~9.7k spans of the 16 x 4096 workload in one call on the GPU; a
     seeded sample of spans checked against the oracle."""
