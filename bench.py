@@ -7,19 +7,20 @@ merging (spans of 2-8 tokens, 40% effective-length reduction -> 2458 cached
 entries per sequence), then 256 decode steps.  Every 8th decode step each
 sequence merges a freshly completed span of n = 2..4 tokens (merge module ->
 roll back n-1 entries -> append the surrogate's K/V); the other steps append
-the new token's K/V.  Every step ends with decode attention over the
-compacted paged cache (16-token pages).
+the new token's K/V.  The append and the step's decode attention over the
+compacted paged cache (16-token pages) are one fused launch
+(sm_decode_step).
 
 One benchmark step runs that whole job for R resident batches ("replicas")
 of 16 sequences, served round-robin the way a server alternates between
 batches; R * (bytes per attention launch) is several times the 256 MB
 Infinity Cache, so no attention launch finds its KV in the MALL.
 
-Printed: one JSON line with the whole-job decode throughput, the decode
-attention kernel's achieved HBM bandwidth against the 8 TB/s roofline
-(measured live with HIP events on the launch stream around each decode
-step's back-to-back attention launches), and the CPU oracle timed on a
-bounded sample of the same job.
+Printed: one JSON line with the whole-job decode throughput, the fused
+append + decode attention kernel's achieved HBM bandwidth against the 8 TB/s
+roofline (measured live with HIP events on the launch stream around each
+decode step's back-to-back launches), and the CPU oracle timed on a bounded
+sample of the same job.
 """
 from __future__ import annotations
 
@@ -148,45 +149,54 @@ class Job:
                                  ("Q", "W_kv", "b_kv", "g_kv", "beta_kv", "W_o", "b_o", "g_o", "beta_o")))
         self.descs = [C.byref(c.desc) for c in self.caches]
 
-    def decode_bytes(self, lens):
-        """Algorithmic HBM bytes of one attention launch over lengths `lens`:
-        K and V of every cached entry, the queries, the outputs and the block
-        table entries read."""
+    def decode_bytes(self, lens, fused=True):
+        """Algorithmic HBM bytes of one fused step launch ending at lengths
+        `lens`: K and V of every entry attended to (the cached ones from the
+        pool, the appended one from its input row), the appended rows'
+        stores, the queries, the outputs and the block table entries read
+        (fused=False: a plain attention launch, no stores)."""
         w = self.w
         es = 2
-        kv = 2 * int(np.sum(lens)) * w.num_kv_heads * w.head_dim * es
+        row = w.num_kv_heads * w.head_dim * es
+        kv = 2 * int(np.sum(lens)) * row
+        new_rows = 2 * w.batch * row if fused else 0
         qo = 2 * w.batch * w.num_q_heads * w.head_dim * es
         bt = 4 * int(np.sum(-(-lens // w.block_size)))
-        return kv + qo + bt
+        return kv + new_rows + qo + bt
 
-    def _update(self, r, s, st):
-        """Cache update of batch r before decode step s: a decode-time merge
-        (merge module, roll back n-1 entries, append the surrogate's K/V) or
-        the new token's K/V."""
+    def _merge(self, r, s, st):
+        """Decode-time merge of batch r before decode step s: the merge
+        module on each sequence's freshly completed span and the roll back of
+        its n-1 entries (the surrogate's K/V is then the step's appended row)."""
         L, w = self.L, self.w
         B, bf = w.batch, self.sm.SM_BF16
-        d = self.descs[r]
-        j = s % self.nin
-        m = self.dmerge.get(s)
-        rc = 0
-        if m is not None:
-            rc |= L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], m["row_idx"].data_ptr(), m["rows"],
-                                   m["offs"].data_ptr(), B, C.byref(self.mp), bf, self.zdec.data_ptr(),
-                                   self.dmerge_ws.data_ptr(), self.dmerge_ws.numel(), self.err.data_ptr(), st)
-            rc |= L.sm_kv_rollback(d, self.ids.data_ptr(), m["k"].data_ptr(), B, st)
-        rc |= L.sm_kv_append(d, self.ids.data_ptr(), self.one_row.data_ptr(), B, B,
-                             self.Kt[j].data_ptr(), self.Vt[j].data_ptr(), st)
+        m = self.dmerge[s]
+        rc = L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], m["row_idx"].data_ptr(), m["rows"],
+                              m["offs"].data_ptr(), B, C.byref(self.mp), bf, self.zdec.data_ptr(),
+                              self.dmerge_ws.data_ptr(), self.dmerge_ws.numel(), self.err.data_ptr(), st)
+        rc |= L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), m["k"].data_ptr(), B, st)
         if rc:
-            raise RuntimeError(f"cache update launch failed at step {s}: {rc}")
+            raise RuntimeError(f"decode-time merge launch failed at step {s}: {rc}")
+
+    def _step(self, r, s, st):
+        """Decode step s of batch r: append the step's K/V row (new token or
+        surrogate) and attend, in one launch."""
+        L, w = self.L, self.w
+        j = s % self.nin
+        rc = L.sm_decode_step(self.descs[r], self.ids.data_ptr(), w.batch, self.Kt[j].data_ptr(),
+                              self.Vt[j].data_ptr(), self.q[j].data_ptr(), w.num_q_heads, w.head_dim ** -0.5,
+                              self.max_len, self.out.data_ptr(), self.dec_ws.data_ptr(), self.dec_ws.numel(), st)
+        if rc:
+            raise RuntimeError(f"decode step launch failed at step {s}: {rc}")
 
     def run(self, stream, upd_stream, events=None):
         """One benchmark step: the whole job for every resident batch.
 
-        Decode attention runs on `stream`; cache updates run on `upd_stream`,
-        each waiting only for its own batch's previous attention.  When both
-        are the same stream every update and every attention runs in order
-        (the default); with two streams batch r's update overlaps the
-        attention launches of the other batches."""
+        Fused decode steps run on `stream`; prompt compression and
+        decode-time merges run on `upd_stream`, each waiting only for its own
+        batch's previous step.  When both are the same stream everything runs
+        in order (the default); with two streams batch r's merge overlaps
+        the decode steps of the other batches."""
         import torch
         L, w = self.L, self.w
         B, bf = w.batch, self.sm.SM_BF16
@@ -194,7 +204,7 @@ class Job:
         overlap = sa != sb
         R = self.R
         # prompt compression of every batch (after its previous job's last
-        # attention), then the first decode step's update
+        # decode step)
         for r in range(R):
             c, dp = self.caches[r], self.dev_prompts[r]
             if overlap:
@@ -216,32 +226,26 @@ class Job:
                                  self.Kp.data_ptr(), self.Vp.data_ptr(), sb)
             if rc:
                 raise RuntimeError(f"prompt compression launch failed: {rc}")
-            self._update(r, 0, sb)
             if overlap:
                 self.upd_done[r].record(upd_stream)
         for s in range(w.decode_steps):
-            j = s % self.nin
+            if s in self.dmerge:
+                for r in range(R):
+                    if overlap:
+                        upd_stream.wait_event(self.attn_done[r])
+                    self._merge(r, s, sb)
+                    if overlap:
+                        self.upd_done[r].record(upd_stream)
             if events is not None:
                 events[0][s].record(stream)
             for r in range(R):
                 if overlap:
                     stream.wait_event(self.upd_done[r])
-                rc = L.sm_decode_attention(self.descs[r], self.ids.data_ptr(), B, self.q[j].data_ptr(),
-                                           w.num_q_heads, w.head_dim ** -0.5, self.max_len, self.out.data_ptr(),
-                                           self.dec_ws.data_ptr(), self.dec_ws.numel(), sa)
-                if rc:
-                    raise RuntimeError(f"attention launch failed at step {s}: {rc}")
+                self._step(r, s, sa)
                 if overlap:
                     self.attn_done[r].record(stream)
             if events is not None:
                 events[1][s].record(stream)
-            if s + 1 < w.decode_steps:
-                for r in range(R):
-                    if overlap:
-                        upd_stream.wait_event(self.attn_done[r])
-                    self._update(r, s + 1, sb)
-                    if overlap:
-                        self.upd_done[r].record(upd_stream)
 
     def check_errors(self):
         bits = [c.error_bits() for c in self.caches] + [int(self.err.item())]
@@ -297,7 +301,7 @@ def extras_report(job, stream, attn_us):
             L.sm_decode_attention(d, ids.data_ptr(), B, job.q[0].data_ptr(), Hq, D ** -0.5, Lu,
                                   job.out.data_ptr(), ws.data_ptr(), ws.numel(), st)
     ms = _time(attn_all, stream, 16) / job.R
-    ubytes = job.decode_bytes(np.full(B, Lu))
+    ubytes = job.decode_bytes(np.full(B, Lu), fused=False)
     out["uncompressed_control"] = {
         "cache_len": Lu, "avg_launch_us": round(ms * 1e3, 3),
         "achieved_GBps": round(ubytes / (ms * 1e-3) / 1e9, 1),
@@ -584,8 +588,8 @@ def main():
             "block_size": w.block_size,
         },
         "roofline": {
-            "kernel": "decode_split_bf16<128>: one launch per decode step and batch; HIP events around "
-                      "each step's back-to-back launches, divided by the launch count",
+            "kernel": "decode_split_bf16<128, step>: one fused append + attention launch per decode step and "
+                      "batch; HIP events around each step's back-to-back launches, divided by the launch count",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": PEAK_HBM_GBS,

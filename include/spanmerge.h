@@ -288,6 +288,31 @@ sm_status sm_decode_attention(const sm_paged_cache *c, const int32_t *seq_ids,
                               float scale, int max_len, void *out, void *ws,
                               size_t ws_bytes, hipStream_t stream);
 
+/*
+ * sm_decode_step -- one decode step of a batch in a single launch: the new
+ * token's K/V row of every sequence is appended and each sequence's new
+ * query attends over its cache including that row (the per-step cache
+ * growth and attention of "Efficiency Analysis").  Same results, cache
+ * state and error bits as
+ *   sm_kv_append(c, seq_ids, {0, 1, ..., n}, n, n, K, V)
+ *   sm_decode_attention(c, seq_ids, n, q, num_q_heads, scale, max_len, ...)
+ * issued back to back, up to the rounding order of the attention sums.  If
+ * the append fails (or the error word was already set) the cache is left
+ * as it was and the attention runs over it unchanged.
+ *
+ *  seq_ids      [n] distinct ids, n <= 256
+ *  K, V         [n][num_kv_heads][head_dim] (cache dtype): the new rows
+ *  q, out, num_q_heads, scale: as sm_decode_attention
+ *  max_len      (host) upper bound on the lengths after the append
+ *  ws, ws_bytes as sm_decode_attention (the same workspace may serve both
+ *               calls, one at a time); n * num_kv_heads <= 65534
+ * Device errors: those of sm_kv_append, then those of sm_decode_attention.
+ */
+sm_status sm_decode_step(const sm_paged_cache *c, const int32_t *seq_ids,
+                         int n, const void *K, const void *V, const void *q,
+                         int num_q_heads, float scale, int max_len, void *out,
+                         void *ws, size_t ws_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

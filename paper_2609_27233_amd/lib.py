@@ -25,7 +25,7 @@ _P, _I, _L, _F, _Z = C.c_void_p, C.c_int, C.c_int64, C.c_float, C.c_size_t
 
 EXPORTED = ("sm_status_string", "sm_merge_workspace_bytes", "sm_merge_spans",
             "sm_pack_spans", "sm_kv_rollback", "sm_kv_append",
-            "sm_decode_workspace_bytes", "sm_decode_attention")
+            "sm_decode_workspace_bytes", "sm_decode_attention", "sm_decode_step")
 
 
 class MergeParams(C.Structure):
@@ -77,6 +77,9 @@ def load(path: str = LIB_PATH):
     L.sm_decode_attention.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _I, _F,
                                       _I, _P, _P, _Z, _P]
     L.sm_decode_attention.restype = _I
+    L.sm_decode_step.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _P, _P, _I, _F,
+                                 _I, _P, _P, _Z, _P]
+    L.sm_decode_step.restype = _I
     _lib = L
     return L
 
@@ -212,3 +215,15 @@ def decode_attention(cache: PagedCache, seq_ids, q, out, ws, max_len: int,
                                     max_len, _ptr(out), _ptr(ws),
                                     ws.numel() * ws.element_size(), _stream(stream))
     _check(st, "sm_decode_attention")
+
+
+def decode_step(cache: PagedCache, seq_ids, K, V, q, out, ws, max_len: int,
+                scale: Optional[float] = None, stream=None):
+    """Append one K/V row per sequence and attend, in one launch: the same
+    as kv_append(cache, seq_ids, arange(n + 1), K, V) then decode_attention."""
+    n, Hq, D = q.shape
+    sc = D ** -0.5 if scale is None else scale
+    st = load().sm_decode_step(C.byref(cache.desc), _ptr(seq_ids), n, _ptr(K), _ptr(V), _ptr(q), Hq, sc,
+                               max_len, _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
+                               _stream(stream))
+    _check(st, "sm_decode_step")

@@ -65,6 +65,7 @@ def test_cache_descriptor_checks(L, kw):
     assert L.sm_kv_rollback(C.byref(d), 1, 1, 1, None) == sm.SM_EINVAL
     assert L.sm_kv_append(C.byref(d), 1, 1, 1, 1, 1, 1, None) == sm.SM_EINVAL
     assert L.sm_decode_attention(C.byref(d), 1, 1, 1, 8, 1.0, 16, 1, 1, 1 << 30, None) == sm.SM_EINVAL
+    assert L.sm_decode_step(C.byref(d), 1, 1, 1, 1, 1, 8, 1.0, 16, 1, 1, 1 << 30, None) == sm.SM_EINVAL
 
 
 def test_request_count_and_workspace_checks(L):
@@ -77,6 +78,13 @@ def test_request_count_and_workspace_checks(L):
     assert need > 0
     assert L.sm_decode_attention(C.byref(d), 1, 1, 1, 32, 1.0, 256, 1, 1, need - 1, None) == sm.SM_EINVAL
     assert L.sm_decode_attention(C.byref(d), 1, 1, 1, 32, 1.0, 257, 1, 1, 1 << 30, None) == sm.SM_EINVAL  # > capacity
+    # the fused step: at most 256 requests, new rows required, same workspace rule
+    assert L.sm_decode_step(C.byref(d), 1, 0, None, None, 1, 32, 1.0, 256, 1, 1, 1 << 30, None) == sm.SM_OK
+    assert L.sm_decode_step(C.byref(d), 1, 257, 1, 1, 1, 32, 1.0, 256, 1, 1, 1 << 30, None) == sm.SM_EINVAL
+    assert L.sm_decode_step(C.byref(d), 1, 1, None, 1, 1, 32, 1.0, 256, 1, 1, 1 << 30, None) == sm.SM_EINVAL
+    assert L.sm_decode_step(C.byref(d), 1, 1, 1, None, 1, 32, 1.0, 256, 1, 1, 1 << 30, None) == sm.SM_EINVAL
+    assert L.sm_decode_step(C.byref(d), 1, 1, 1, 1, 1, 32, 1.0, 256, 1, 1, need - 1, None) == sm.SM_EINVAL
+    assert L.sm_decode_step(C.byref(d), 1, 1, 1, 1, 1, 32, 1.0, 257, 1, 1, 1 << 30, None) == sm.SM_EINVAL
 
 
 def test_merge_argument_checks(L):
