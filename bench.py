@@ -40,12 +40,12 @@ PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 METRIC = "decode-attention tokens/s + achieved HBM GB/s over span-compacted KV cache"
 
-# HBM traffic of the attention kernel from rocprofv3 --pmc FETCH_SIZE and
-# WRITE_SIZE runs (see profiles/decode_attention_llama3-8b-layer.md): scaled
+# HBM traffic of the fused step kernel from rocprofv3 --pmc FETCH_SIZE and
+# WRITE_SIZE runs (see profiles/decode_step_llama3-8b-layer.md): scaled
 # measured bytes per launch divided by the algorithmic bytes of the same
 # launches.  Valid only for the kernel source it was measured on.
-TRAFFIC_RATIO = 1.0117
-TRAFFIC_SOURCE_SHA256 = {"decode_attn.hip": "1f971b6ca0b21e17bf9563b22717234d3f8ff67624ceb07051d24c7d3031a4fd", "common.hpp": "12a4a21e0b0bf50c3716cc96b5c366317e63901b1eb3601120fe353d7d9bfbb6"}
+TRAFFIC_RATIO = 1.0154
+TRAFFIC_SOURCE_SHA256 = {"decode_attn.hip": "b1289901dddb192d4f0d65dca7779bfd824c9c38dc8c62ac3638b7ea4855cec7", "common.hpp": "12a4a21e0b0bf50c3716cc96b5c366317e63901b1eb3601120fe353d7d9bfbb6"}
 
 
 def log(*a):
@@ -279,6 +279,27 @@ def extras_report(job, stream, attn_us):
     out = {}
     g = wl.generator(77, dev)
     ids = job.ids
+
+    # --- the attention kernel alone (no append) over the job's caches as the
+    # job left them: the plain decode_attention entry point
+    descs0 = [C.byref(c.desc) for c in job.caches]
+    ws0 = torch.zeros(sm.decode_workspace_bytes(B, Hq, D, job.max_len), dtype=torch.uint8, device=dev)
+
+    def attn_job():
+        for d0 in descs0:
+            L.sm_decode_attention(d0, ids.data_ptr(), B, job.q[0].data_ptr(), Hq, D ** -0.5, job.max_len,
+                                  job.out.data_ptr(), ws0.data_ptr(), ws0.numel(), st)
+    ms0 = _time(attn_job, stream, 16) / job.R
+    lens_end = job.caches[0].lengths[:B].cpu().numpy().astype(np.int64)
+    b0 = job.decode_bytes(lens_end, fused=False)
+    out["attention_only"] = {
+        "kernel": "decode_split_bf16<128> (decode_attention, no append)",
+        "mean_cache_len": round(float(lens_end.mean()), 1), "avg_launch_us": round(ms0 * 1e3, 3),
+        "achieved_GBps": round(b0 / (ms0 * 1e-3) / 1e9, 1), "frac": round(b0 / (ms0 * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "note": "the plain attention kernel over the same caches at the end of the job; HIP events around "
+                "back-to-back launches"}
+    del ws0
+    log("extras: attention-only done")
 
     # --- uncompressed control: same launch shape, cache length = prompt + 128
     Lu = w.prompt_len + 128
