@@ -526,8 +526,8 @@ __global__ __launch_bounds__(256) void gemm_f32_nt_gelu(const float *__restrict_
 }
 
 // ---------------------------------------------------------------------------
-// Pooling: one workgroup per span.  Thread t owns the 16-byte column groups
-// t, t + 256, ... of every row.
+// Pooling, general form (any d the call accepts): one workgroup per span.
+// Thread t owns the 16-byte column groups t, t + 256, ... of every row.
 
 constexpr int kPoolThreads = 256;
 constexpr int kMaxSpanLen = 256;
@@ -542,6 +542,20 @@ struct Vec {
 template <typename T>
 __device__ __forceinline__ void load_vec(const T *p, float *x) {
   const u32x4_t u = *(const u32x4_t *)p;
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(u[e] << 16);
+      x[2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = __uint_as_float(u[e]);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void unpack_vec(u32x4_t u, float *x) {
   if constexpr (sizeof(T) == 2) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -710,7 +724,178 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const T *__restrict_
   }
 }
 
-// LN_o over fp32 rows Y -> out (storage dtype)
+// Pooling, register form for d = NCH * 64 * (16 / sizeof(T)): one workgroup of
+// four waves per span.  Wave w takes rows w, w + 4, ... of the span whole into
+// its registers (lane l holds the 16-byte groups l, l + 64, ... of the row), so
+// a row's LN statistics and its h head scores cost one load round trip and
+// wave reductions only.  The LN_kv gain, bias and the queries are staged once
+// in LDS.  The weighted sum then splits the columns over the workgroup and
+// re-reads the span's rows (cache hits), four rows per round trip.
+constexpr int kPoolWaves = 4;
+
+template <typename T, int NCH>
+__global__ __launch_bounds__(kPoolWaves * 64) void pool_rows_kernel(const T *__restrict__ G1,
+                                                                    const int32_t *__restrict__ span_offsets,
+                                                                    int num_spans, int total_rows,
+                                                                    const T *__restrict__ Q,
+                                                                    const T *__restrict__ g_kv,
+                                                                    const T *__restrict__ beta_kv, float eps, int d,
+                                                                    int h, T *__restrict__ cout, int32_t *err) {
+  constexpr int VN = Vec<T>::N;
+  constexpr int NT = kPoolWaves * 64, NV = NCH * 64;
+  __shared__ float alpha[kMaxSpanLen][kMaxHeads];
+  __shared__ float row_mean[kMaxSpanLen], row_inv[kMaxSpanLen];
+  __shared__ u32x4_t par[3][NV];  // g_kv, beta_kv, Q as stored
+  const int s = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  T *dst = cout + (int64_t)s * d;
+
+  const int r0 = span_offsets[s], r1 = span_offsets[s + 1];
+  const int n = r1 - r0;
+  bool ok = n >= 1 && n <= kMaxSpanLen && r0 >= 0 && r1 <= total_rows;
+  if (s == 0 && r0 != 0) ok = false;
+  if (s == num_spans - 1 && r1 != total_rows) ok = false;
+  if (!ok) {
+    if (tid == 0) set_err(err, SM_ERR_EINVAL);
+    for (int v = tid; v < NV; v += NT) ((u32x4_t *)dst)[v] = u32x4_t{0u, 0u, 0u, 0u};
+    return;
+  }
+  const int dh = d / h;
+  const float inv_sqrt_dh = 1.0f / sqrtf((float)dh);
+
+  // this wave's first row is requested before the parameters are staged
+  u32x4_t xr[NCH];
+  if (w < n) {
+    const u32x4_t *row = (const u32x4_t *)(G1 + (int64_t)(r0 + w) * d);
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) xr[u] = row[u * 64 + lane];
+  }
+  for (int v = tid; v < NV; v += NT) {
+    par[0][v] = ((const u32x4_t *)g_kv)[v];
+    par[1][v] = ((const u32x4_t *)beta_kv)[v];
+    par[2][v] = ((const u32x4_t *)Q)[v];
+  }
+  int hd[NCH];  // head of this lane's group in chunk u (a group never straddles heads)
+#pragma unroll
+  for (int u = 0; u < NCH; ++u) hd[u] = ((u * 64 + lane) * VN) / dh;
+  __syncthreads();
+
+  for (int j = w; j < n; j += kPoolWaves) {
+    // keeps the parameter reads below inside the loop: hoisted, they would
+    // hold 3 * NCH * VN floats live across it
+    asm volatile("" ::: "memory");
+    if (j != w) {
+      const u32x4_t *row = (const u32x4_t *)(G1 + (int64_t)(r0 + j) * d);
+#pragma unroll
+      for (int u = 0; u < NCH; ++u) xr[u] = row[u * 64 + lane];
+    }
+    float x[NCH][VN];
+    float sum = 0.f;
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      unpack_vec<T>(xr[u], x[u]);
+#pragma unroll
+      for (int e = 0; e < VN; ++e) sum += x[u][e];
+    }
+    const float mean = wave_sum(sum) / d;
+    float sq = 0.f;
+#pragma unroll
+    for (int u = 0; u < NCH; ++u)
+#pragma unroll
+      for (int e = 0; e < VN; ++e) sq += (x[u][e] - mean) * (x[u][e] - mean);
+    const float inv = 1.0f / sqrtf(wave_sum(sq) / d + eps);
+    float part[NCH];
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      float gv[VN], bv[VN], qv[VN];
+      unpack_vec<T>(par[0][u * 64 + lane], gv);
+      unpack_vec<T>(par[1][u * 64 + lane], bv);
+      unpack_vec<T>(par[2][u * 64 + lane], qv);
+      float p = 0.f;
+#pragma unroll
+      for (int e = 0; e < VN; ++e) p += (gv[e] * (x[u][e] - mean) * inv + bv[e]) * qv[e];
+      part[u] = p;
+    }
+#pragma unroll 1
+    for (int i = 0; i < h; ++i) {
+      float t = 0.f;
+#pragma unroll
+      for (int u = 0; u < NCH; ++u) t += hd[u] == i ? part[u] : 0.f;
+      t = wave_sum(t);
+      if (lane == 0) alpha[j][i] = t * inv_sqrt_dh;  // raw score for now
+    }
+    if (lane == 0) {
+      row_mean[j] = mean;
+      row_inv[j] = inv;
+    }
+  }
+  __syncthreads();
+  // softmax over the span, per head
+  if (tid < h) {
+    float m = -INFINITY;
+    for (int j = 0; j < n; ++j) m = fmaxf(m, alpha[j][tid]);
+    float z = 0.f;
+    for (int j = 0; j < n; ++j) {
+      const float e = expf(alpha[j][tid] - m);
+      alpha[j][tid] = e;
+      z += e;
+    }
+    const float iz = 1.0f / z;
+    for (int j = 0; j < n; ++j) alpha[j][tid] *= iz;
+  }
+  __syncthreads();
+
+  // c = sum_j alpha_j P_j over this thread's column groups
+  for (int v = tid; v < NV; v += NT) {
+    const int col = v * VN, head = col / dh;
+    float gv[VN], bv[VN], acc[VN];
+    unpack_vec<T>(par[0][v], gv);
+    unpack_vec<T>(par[1][v], bv);
+#pragma unroll
+    for (int e = 0; e < VN; ++e) acc[e] = 0.f;
+    for (int j0 = 0; j0 < n; j0 += 4) {
+      u32x4_t xq[4];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        if (j0 + jj < n) xq[jj] = *(const u32x4_t *)(G1 + (int64_t)(r0 + j0 + jj) * d + col);
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        if (j0 + jj < n) {
+          float x[VN];
+          unpack_vec<T>(xq[jj], x);
+          const float a = alpha[j0 + jj][head], mean = row_mean[j0 + jj], inv = row_inv[j0 + jj];
+#pragma unroll
+          for (int e = 0; e < VN; ++e) acc[e] += a * (gv[e] * (x[e] - mean) * inv + bv[e]);
+        }
+    }
+    store_vec(dst + col, acc);
+  }
+}
+
+template <typename T>
+static hipError_t launch_pool(const T *G1, const int32_t *span_offsets, int num_spans, int total_rows, const T *Q,
+                              const T *g_kv, const T *beta_kv, float eps, int d, int h, T *cout, int32_t *err,
+                              hipStream_t stream) {
+  constexpr int VN = Vec<T>::N;
+  const int nch = d % (64 * VN) == 0 ? d / (64 * VN) : 0;
+#define SM_POOL_CASE(C)                                                                                          \
+  case C:                                                                                                        \
+    hipLaunchKernelGGL((pool_rows_kernel<T, C>), dim3(num_spans), dim3(kPoolWaves * 64), 0, stream, G1,          \
+                       span_offsets, num_spans, total_rows, Q, g_kv, beta_kv, eps, d, h, cout, err);             \
+    break;
+  switch (nch) {
+    SM_POOL_CASE(1) SM_POOL_CASE(2) SM_POOL_CASE(3) SM_POOL_CASE(4)
+    SM_POOL_CASE(5) SM_POOL_CASE(6) SM_POOL_CASE(7) SM_POOL_CASE(8)
+    SM_POOL_CASE(16)
+    default:
+      hipLaunchKernelGGL(pool_kernel<T>, dim3(num_spans), dim3(kPoolThreads), 0, stream, G1, span_offsets,
+                         num_spans, total_rows, Q, g_kv, beta_kv, eps, d, h, cout, err);
+  }
+#undef SM_POOL_CASE
+  return hipGetLastError();
+}
+
+// LN_o over fp32 rows Y -> out (storage dtype), one workgroup per row; the
+// row, the gain and the bias are all requested before the first reduction.
 template <typename T>
 __global__ __launch_bounds__(kPoolThreads) void ln_rows_kernel(const float *__restrict__ Y,
                                                                const T *__restrict__ g, const T *__restrict__ b,
@@ -720,37 +905,53 @@ __global__ __launch_bounds__(kPoolThreads) void ln_rows_kernel(const float *__re
   const int s = blockIdx.x, tid = threadIdx.x;
   const int nvec = d / 4;
   const float *row = Y + (int64_t)s * d;
-  float x[kMaxV][4];
-  float sum = 0.f;
+  float x[kMaxV][4], gv[kMaxV][4], bv[kMaxV][4];
 #pragma unroll
   for (int u = 0; u < kMaxV; ++u) {
     const int v = tid + u * kPoolThreads;
     if (v < nvec) {
       load_vec<float>(row + v * 4, x[u]);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) sum += x[u][e];
+      if constexpr (sizeof(T) == 2) {
+        const uint2 gg = *(const uint2 *)(g + v * 4), bb = *(const uint2 *)(b + v * 4);
+        gv[u][0] = __uint_as_float(gg.x << 16);
+        gv[u][1] = __uint_as_float(gg.x & 0xffff0000u);
+        gv[u][2] = __uint_as_float(gg.y << 16);
+        gv[u][3] = __uint_as_float(gg.y & 0xffff0000u);
+        bv[u][0] = __uint_as_float(bb.x << 16);
+        bv[u][1] = __uint_as_float(bb.x & 0xffff0000u);
+        bv[u][2] = __uint_as_float(bb.y << 16);
+        bv[u][3] = __uint_as_float(bb.y & 0xffff0000u);
+      } else {
+        load_vec<float>((const float *)g + v * 4, gv[u]);
+        load_vec<float>((const float *)b + v * 4, bv[u]);
+      }
     }
   }
+  float sum = 0.f;
+#pragma unroll
+  for (int u = 0; u < kMaxV; ++u)
+    if (tid + u * kPoolThreads < nvec)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sum += x[u][e];
   const float mean = block_sum(sum, red) / d;
   float sq = 0.f;
 #pragma unroll
-  for (int u = 0; u < kMaxV; ++u) {
-    const int v = tid + u * kPoolThreads;
-    if (v < nvec)
+  for (int u = 0; u < kMaxV; ++u)
+    if (tid + u * kPoolThreads < nvec)
 #pragma unroll
       for (int e = 0; e < 4; ++e) sq += (x[u][e] - mean) * (x[u][e] - mean);
-  }
   const float inv = 1.0f / sqrtf(block_sum(sq, red) / d + eps);
 #pragma unroll
   for (int u = 0; u < kMaxV; ++u) {
     const int v = tid + u * kPoolThreads;
     if (v < nvec) {
+      float y[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int col = v * 4 + e;
-        const float gg = Elem<T>::load(g + col), bb = Elem<T>::load(b + col);
-        out[(int64_t)s * d + col] = Elem<T>::to_store(gg * (x[u][e] - mean) * inv + bb);
-      }
+      for (int e = 0; e < 4; ++e) y[e] = gv[u][e] * (x[u][e] - mean) * inv + bv[u][e];
+      if constexpr (sizeof(T) == 2)
+        *(uint2 *)(out + (int64_t)s * d + v * 4) = make_uint2(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]));
+      else
+        *(f32x4_t *)(out + (int64_t)s * d + v * 4) = f32x4_t{y[0], y[1], y[2], y[3]};
     }
   }
 }
@@ -806,11 +1007,10 @@ SM_API sm_status sm_merge_spans(const void *emb, int64_t emb_rows, const int32_t
                          stream, (const uint16_t *)emb, row_idx, emb_rows, (const uint16_t *)p->W_kv,
                          (const uint16_t *)p->b_kv, (uint16_t *)g1, total_rows, d, d, err);
     if (hipGetLastError() != hipSuccess) return SM_EHIP;
-    hipLaunchKernelGGL(pool_kernel<uint16_t>, dim3(num_spans), dim3(kPoolThreads), 0, stream,
-                       (const uint16_t *)g1, span_offsets, num_spans, total_rows, (const uint16_t *)p->Q,
-                       (const uint16_t *)p->g_kv, (const uint16_t *)p->beta_kv, p->ln_eps, d, h,
-                       (uint16_t *)cbuf, err);
-    if (hipGetLastError() != hipSuccess) return SM_EHIP;
+    if (launch_pool<uint16_t>((const uint16_t *)g1, span_offsets, num_spans, total_rows, (const uint16_t *)p->Q,
+                              (const uint16_t *)p->g_kv, (const uint16_t *)p->beta_kv, p->ln_eps, d, h,
+                              (uint16_t *)cbuf, err, stream) != hipSuccess)
+      return SM_EHIP;
     if (num_spans <= kSkinnyMaxM)
       launch_skinny<float>((const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
                            (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, ybuf, num_spans, d, d, err, stream);
@@ -831,10 +1031,10 @@ SM_API sm_status sm_merge_spans(const void *emb, int64_t emb_rows, const int32_t
                        (const float *)emb, row_idx, emb_rows, (const float *)p->W_kv, (const float *)p->b_kv,
                        (float *)g1, total_rows, d, d, err);
     if (hipGetLastError() != hipSuccess) return SM_EHIP;
-    hipLaunchKernelGGL(pool_kernel<float>, dim3(num_spans), dim3(kPoolThreads), 0, stream, (const float *)g1,
-                       span_offsets, num_spans, total_rows, (const float *)p->Q, (const float *)p->g_kv,
-                       (const float *)p->beta_kv, p->ln_eps, d, h, (float *)cbuf, err);
-    if (hipGetLastError() != hipSuccess) return SM_EHIP;
+    if (launch_pool<float>((const float *)g1, span_offsets, num_spans, total_rows, (const float *)p->Q,
+                           (const float *)p->g_kv, (const float *)p->beta_kv, p->ln_eps, d, h, (float *)cbuf, err,
+                           stream) != hipSuccess)
+      return SM_EHIP;
     hipLaunchKernelGGL(gemm_f32_nt_gelu, dim3(d / kFT, (num_spans + kFT - 1) / kFT), dim3(256), 0, stream,
                        (const float *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans, (const float *)p->W_o,
                        (const float *)p->b_o, ybuf, num_spans, d, d, err);

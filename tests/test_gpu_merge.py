@@ -51,9 +51,36 @@ def test_merge_tiny_f32(orc, spread):
     assert e <= TOL[torch.float32]
 
 
-@pytest.mark.parametrize("d,S,nmax,spread", [(512, 300, 8, True), (1024, 129, 5, False),
-                                             (768, 37, 12, True), (256, 1, 1, True)])
-def test_merge_bf16_small(orc, d, S, nmax, spread):
+@pytest.mark.parametrize("d,S,nmax,h", [(512, 50, 9, 8), (1024, 20, 5, 16), (768, 17, 3, 4)])
+def test_merge_f32_heads(orc, d, S, nmax, h):
+    """fp32 storage at several widths and head counts (768 takes the
+    register form at 3 groups per lane)."""
+    rng = np.random.RandomState(7 * d + S)
+    lens = rng.randint(1, nmax + 1, size=S)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    vocab = 500
+    row_idx = rng.randint(0, vocab, size=int(offs[-1])).astype(np.int32)
+    g = wl.generator(d + h)
+    emb = wl.randn((vocab, d), torch.float32, g, std=0.02)
+    params = wl.make_merge_params(d, h, torch.float32, g, spread=True)
+    say("merge f32", d, S, nmax, h)
+    out, err = _gpu_merge(emb.to(dev()), row_idx, offs, params, h, torch.float32)
+    assert err == 0
+    ref = _oracle(orc, wl.to_f64(emb), row_idx, offs, params, h)
+    e = rel_l2_max(out.numpy(), ref)
+    say("rel_l2_max", e)
+    assert e <= TOL[torch.float32]
+
+
+@pytest.mark.parametrize("d,S,nmax,spread,h", [(512, 300, 8, True, 4), (1024, 129, 5, False, 4),
+                                               (768, 37, 12, True, 4), (256, 1, 1, True, 4),
+                                               (1024, 60, 6, True, 16), (2048, 40, 8, True, 8),
+                                               (3584, 33, 5, True, 4), (1536, 20, 40, True, 2),
+                                               (8192, 9, 4, True, 1)])
+def test_merge_bf16_small(orc, d, S, nmax, spread, h):
+    """Sizes cover the register-form pooling at 1..8 and 16 groups per lane,
+    one to sixteen heads, spans longer than the four pooling waves, and the
+    general form (d = 256 and 768 are not multiples of 512)."""
     rng = np.random.RandomState(d + S)
     lens = rng.randint(1, nmax + 1, size=S)
     offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
@@ -61,11 +88,11 @@ def test_merge_bf16_small(orc, d, S, nmax, spread):
     row_idx = rng.randint(0, vocab, size=int(offs[-1])).astype(np.int32)
     g = wl.generator(d)
     emb = wl.randn((vocab, d), torch.bfloat16, g, std=0.02)
-    params = wl.make_merge_params(d, 4, torch.bfloat16, g, spread=spread)
-    say("merge bf16", d, S, nmax, spread)
-    out, err = _gpu_merge(emb.to(dev()), row_idx, offs, params, 4, torch.bfloat16)
+    params = wl.make_merge_params(d, h, torch.bfloat16, g, spread=spread)
+    say("merge bf16", d, S, nmax, spread, h)
+    out, err = _gpu_merge(emb.to(dev()), row_idx, offs, params, h, torch.bfloat16)
     assert err == 0
-    ref = _oracle(orc, wl.to_f64(emb), row_idx, offs, params, 4)
+    ref = _oracle(orc, wl.to_f64(emb), row_idx, offs, params, h)
     e = rel_l2_max(out.float().numpy(), ref)
     say("rel_l2_max", e)
     assert e <= TOL[torch.bfloat16]
