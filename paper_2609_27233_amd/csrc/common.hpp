@@ -103,6 +103,17 @@ __device__ __forceinline__ float wave_max(float v) {
   return fmaxf(a, b);
 }
 
+// Workgroup barrier that orders LDS only.  __syncthreads() also waits for
+// every outstanding global load of the calling wave (vmcnt(0)); this one
+// lets loads whose results are consumed later stay in flight across it.
+// Use it only where no wave reads global data another wave wrote before
+// the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Sum over the workgroup; `red` needs blockDim.x / 64 floats of LDS.
 __device__ __forceinline__ float block_sum(float v, float *red) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;

@@ -142,6 +142,13 @@ __device__ void write_zero_rows(const DecodeArgs &a, int i, int g, int DH, int s
 // Every workgroup calls this once its partial is stored.  The last of the
 // nc workgroups of (sequence i, kv head g) to arrive rescales and sums all
 // partials of the group, writes the output rows and re-arms the counter.
+// The partials are fetched kCombineBatch chunks at a time for all of a
+// thread's output elements in one go (each fetch is a round trip to the
+// coherent level of the memory hierarchy); across batches the running sum
+// is rescaled to the running maximum, so for nc <= kCombineBatch the result
+// is exactly max-then-sum over all chunks.
+constexpr int kCombineBatch = 4;
+
 template <typename OutT>
 __device__ void finish_group(const DecodeArgs &a, int i, int g, int nc, int DH, int *last) {
   int32_t *ctr = a.counters + (int64_t)i * a.Hkv + g;
@@ -152,24 +159,74 @@ __device__ void finish_group(const DecodeArgs &a, int i, int g, int nc, int DH, 
   __syncthreads();
   if (!*last) return;
   OutT *out = (OutT *)a.out;
-  for (int e = threadIdx.x; e < a.G * DH; e += blockDim.x) {
-    const int hh = e / DH, dd = e - hh * DH;
-    const int64_t base = ((int64_t)i * a.Hq + g * a.G + hh) * a.max_chunks;
-    float M = -INFINITY;
-    bool bad = false;
-    for (int c = 0; c < nc; ++c) {
-      bad |= get_partial(&a.ws_ml[(base + c) * 2 + 1]) < 0.f;
-      M = fmaxf(M, get_partial(&a.ws_ml[(base + c) * 2 + 0]));
+  constexpr int kPer = 2;  // output elements per thread and pass
+  const int ne = a.G * DH;
+  for (int e0 = 0; e0 < ne; e0 += kPer * kDecThreads) {
+    float M[kPer], acc[kPer], ls[kPer];
+    bool bad[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      M[k] = -INFINITY;
+      acc[k] = 0.f;
+      ls[k] = 0.f;
+      bad[k] = false;
     }
-    float acc = 0.f, ls = 0.f;
-    if (!bad) {
-      for (int c = 0; c < nc; ++c) {
-        const float f = exp2f(get_partial(&a.ws_ml[(base + c) * 2 + 0]) - M);
-        acc += get_partial(&a.ws_o[(base + c) * DH + dd]) * f;
-        ls += get_partial(&a.ws_ml[(base + c) * 2 + 1]) * f;
+    for (int c0 = 0; c0 < nc; c0 += kCombineBatch) {
+      float pm[kPer][kCombineBatch], pl[kPer][kCombineBatch], po[kPer][kCombineBatch];
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+#pragma unroll
+        for (int cc = 0; cc < kCombineBatch; ++cc) {
+          pm[k][cc] = -INFINITY;
+          pl[k][cc] = 0.f;
+          po[k][cc] = 0.f;
+        }
+        const int e = e0 + threadIdx.x + kDecThreads * k;
+        if (e < ne) {
+          const int hh = e / DH, dd = e - hh * DH;
+          const int64_t base = ((int64_t)i * a.Hq + g * a.G + hh) * a.max_chunks + c0;
+#pragma unroll
+          for (int cc = 0; cc < kCombineBatch; ++cc)
+            if (c0 + cc < nc) {
+              pm[k][cc] = get_partial(&a.ws_ml[(base + cc) * 2 + 0]);
+              pl[k][cc] = get_partial(&a.ws_ml[(base + cc) * 2 + 1]);
+              po[k][cc] = get_partial(&a.ws_o[(base + cc) * DH + dd]);
+            }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        float Mb = M[k];
+#pragma unroll
+        for (int cc = 0; cc < kCombineBatch; ++cc)
+          if (c0 + cc < nc) {
+            bad[k] |= pl[k][cc] < 0.f;
+            Mb = fmaxf(Mb, pm[k][cc]);
+          }
+        if (M[k] != -INFINITY && Mb != M[k]) {  // rescale what earlier batches summed
+          const float r = exp2f(M[k] - Mb);
+          acc[k] *= r;
+          ls[k] *= r;
+        }
+        M[k] = Mb;
+#pragma unroll
+        for (int cc = 0; cc < kCombineBatch; ++cc)
+          if (c0 + cc < nc) {
+            const float f = pm[k][cc] == -INFINITY ? 0.f : exp2f(pm[k][cc] - Mb);
+            acc[k] += po[k][cc] * f;
+            ls[k] += pl[k][cc] * f;
+          }
       }
     }
-    out[((int64_t)i * a.Hq + g * a.G + hh) * DH + dd] = Elem<OutT>::to_store(bad || !(ls > 0.f) ? 0.f : acc / ls);
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int e = e0 + threadIdx.x + kDecThreads * k;
+      if (e < ne) {
+        const int hh = e / DH, dd = e - hh * DH;
+        out[((int64_t)i * a.Hq + g * a.G + hh) * DH + dd] =
+            Elem<OutT>::to_store(bad[k] || !(ls[k] > 0.f) ? 0.f : acc[k] / ls[k]);
+      }
+    }
   }
   if (threadIdx.x == 0) *ctr = 0;
 }
@@ -594,6 +651,15 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
         pages[p] = blk;
       }
     }
+    if (w == kDecWaves - 1) {  // the plan, before this wave issues the new row's loads
+      PlanOut po;
+      plan_regs(a, pr, po);
+      const int pop_i = request_value(po.pop, i);
+      if (lane == 0) {
+        step_plan_sh[0] = po.ok;
+        step_plan_sh[1] = pop_i;
+      }
+    }
     // the new token's score inputs and rows: lane l of wave w takes dims
     // l, l + 64 of query heads w, w + 4, ...
     const uint16_t *kn = (const uint16_t *)a.k_new + ((int64_t)i * a.Hkv + g) * DH;
@@ -618,20 +684,12 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
       vrow_e = vn[tid];
       vrow = bf16_to_f32(vrow_e);
     }
-    if (w == kDecWaves - 1) {  // the plan, while this wave's loads above are in flight
-      PlanOut po;
-      plan_regs(a, pr, po);
-      const int pop_i = request_value(po.pop, i);
-      if (lane == 0) {
-        step_plan_sh[0] = po.ok;
-        step_plan_sh[1] = pop_i;
-      }
-    }
     {
       const bool wave_bad = __ballot(bad_page) != 0;
       if (lane == 0) step_bad_page[w] = wave_bad;
     }
-    __syncthreads();
+    // the new row's loads stay in flight: they are consumed after the loop
+    lds_barrier();
 #pragma unroll
     for (int ww = 0; ww < kDecWaves; ++ww) pages_ok = pages_ok && !step_bad_page[ww];
   } else {
@@ -787,8 +845,12 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
       float mx = sc[0];
 #pragma unroll
       for (int j = 1; j < 8; ++j) mx = fmaxf(mx, sc[j]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      {
+        float a, b;
+        swap16(mx, a, b);
+        swap32(fmaxf(a, b), a, b);
+        mx = fmaxf(a, b);
+      }
       const float m_new = fmaxf(m_run, mx);  // finite: every tile has a valid token
       const float alpha = exp2f(m_run - m_new);
       float p[8], ps = 0.f;
@@ -835,8 +897,13 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     if constexpr (STEP) step_finish();
 
     // per-head totals of this wave (lanes r, r+16, r+32, r+48 share head r)
-    float l_tot = l_run + __shfl_xor(l_run, 16, 64);
-    l_tot += __shfl_xor(l_tot, 32, 64);
+    float l_tot;
+    {
+      float a, b;
+      swap16(l_run, a, b);
+      swap32(a + b, a, b);
+      l_tot = a + b;
+    }
     if (q4 == 0) {
       red_m[w][r] = m_run;
       red_l[w][r] = l_tot;
