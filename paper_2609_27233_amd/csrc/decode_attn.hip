@@ -454,6 +454,53 @@ __device__ void plan_regs(const DecodeArgs &a, const PlanRegs &pr, PlanOut &po) 
   po.total = total;
 }
 
+// The same plan when every request fits one slot (n <= 64, lane l holds
+// request l): one pass over the earlier requests for duplicates and a
+// single window of popped blocks.  Same outcome as plan_regs.
+__device__ void plan_regs_one(const DecodeArgs &a, const PlanRegs &pr, PlanOut &po) {
+  const int lane = threadIdx.x & 63, n = a.n;
+  const int sk = pr.sk[0], Lk = pr.Lk[0];
+  int dup = 0;
+  for (int j = 0; j < n; ++j) dup |= (j < lane) & (__builtin_amdgcn_readlane(sk, j) == sk);
+  int inval = 0, range = 0, need = 0;
+  if (lane < n) {
+    if (sk < 0 || sk >= a.max_seqs || dup) inval = 1;
+    else if (Lk < 0 || (int64_t)Lk + 1 > a.cap) range = 1;
+    else need = (Lk & ((1 << a.bs_log2) - 1)) == 0;
+  }
+  const bool any_inval = __ballot(inval) != 0;
+  const bool any_range = __ballot(range) != 0;
+  const uint64_t m = __ballot(need);
+  const int incl = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0)) + need;
+  const int total = __popcll(m);
+  const int top = pr.top;
+  int bits = any_inval ? SM_ERR_EINVAL
+             : any_range ? SM_ERR_ERANGE
+             : (top < 0 || top > a.num_blocks || total > top) ? SM_ERR_ENOMEM
+                                                              : 0;
+  const bool go = !pr.frozen && bits == 0;
+  // pop index incl - 1 < total <= n <= 64: an entry of the first window
+  const int blk = __shfl(pr.win[0], (go && need) ? incl - 1 : 0, kWave);
+  const bool popped = go && need;
+  const bool any_stack = __ballot(popped && (blk < 0 || blk >= a.num_blocks)) != 0;
+  if (go && any_stack) bits = SM_ERR_EINVAL;  // corrupt free stack
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    po.need[k] = 0;
+    po.pop[k] = -1;
+  }
+  po.need[0] = need;
+  po.pop[0] = popped ? blk : -1;
+  po.ok = go && !any_stack;
+  po.bits = pr.frozen ? 0 : bits;
+  po.total = total;
+}
+
+__device__ __forceinline__ void plan_any(const DecodeArgs &a, const PlanRegs &pr, PlanOut &po) {
+  if (a.n <= 64) plan_regs_one(a, pr, po);
+  else plan_regs(a, pr, po);
+}
+
 // Value of request i's slot k-array entry (held by lane i % 64) in every lane.
 __device__ __forceinline__ int request_value(const int (&v)[4], int i) {
   const int l = i & 63, q = i >> 6;  // uniform
@@ -476,7 +523,7 @@ __device__ void step_commit_wave(const DecodeArgs &a) {
   step_plan_read1(a, pr);
   step_plan_read2(a, pr);
   PlanOut po;
-  plan_regs(a, pr, po);
+  plan_any(a, pr, po);
   int arrived = 0;
   if (lane == 0) {
     for (int it = 0; it < kCommitSpinLimit; ++it) {
@@ -611,14 +658,23 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     }
     esink = nullptr;  // errors travel with the arrival
     // wave 3 (no page ids to fetch at these sizes) works out the whole
-    // append -- two round trips and register work, about as long as the
-    // other waves' chain of this request's id, length and page ids
+    // append: two round trips and register work, beside the other waves'
+    // chain of this request's id, length and page ids
     if (w == kDecWaves - 1) step_plan_read1(a, pr);
     s = a.seq_ids[i];
     const int frozen = *a.err != 0;
     const bool own_ok = s >= 0 && s < a.max_seqs;
     if (w == kDecWaves - 1) step_plan_read2(a, pr);
     L_pool = own_ok ? a.lengths[s] : 0;
+    if (w == kDecWaves - 1) {  // the plan, as soon as its reads are in
+      PlanOut po;
+      plan_any(a, pr, po);
+      const int pop_i = request_value(po.pop, i);
+      if (lane == 0) {
+        step_plan_sh[0] = po.ok;
+        step_plan_sh[1] = pop_i;
+      }
+    }
     if (!own_ok || L_pool < 0 || L_pool > (a.max_blocks << bs_log2)) st = SM_ERR_EINVAL;
     own_can = !frozen && st == 0 && (int64_t)L_pool + 1 <= a.cap;
     if (st == 0) {  // chunked for the appended length whenever this request can append
@@ -649,15 +705,6 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
           blk = 0;
         }
         pages[p] = blk;
-      }
-    }
-    if (w == kDecWaves - 1) {  // the plan, before this wave issues the new row's loads
-      PlanOut po;
-      plan_regs(a, pr, po);
-      const int pop_i = request_value(po.pop, i);
-      if (lane == 0) {
-        step_plan_sh[0] = po.ok;
-        step_plan_sh[1] = pop_i;
       }
     }
     // the new token's score inputs and rows: lane l of wave w takes dims
@@ -912,7 +959,8 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     for (int dt = 0; dt < DH / 16; ++dt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) red_o[w][r][16 * dt + 4 * q4 + j] = o[dt][j];
-    __syncthreads();
+    // LDS only: the fused step's row stores and arrival need not land first
+    lds_barrier();
 
     for (int e = tid; e < G * DH; e += kDecThreads) {
       const int hh = e / DH, dd = e - hh * DH;

@@ -261,3 +261,37 @@ def test_full_request_count(orc):
     assert_same_state(c, oc)
     _counters_clear(ws)
     assert rel_l2_max(out.float().numpy(), ref) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("n,dup", [(64, None), (65, None), (130, None), (64, (5, 63)), (65, (0, 64)),
+                                   (130, (3, 100)), (130, (70, 129))])
+def test_request_slots_and_duplicates(orc, n, dup):
+    """Request counts at the edges of one 64-request slot per lane (the plan
+    takes a single-slot form up to 64 requests), with and without a repeated
+    id in the same slot or across slots; lengths straddle page edges so that
+    some requests pop a block."""
+    dtype, Hq, H, D, bs = torch.bfloat16, 8, 2, 64, 16
+    rng = np.random.RandomState(1000 + n + (dup[1] if dup else 0))
+    lens = list(rng.randint(0, 70, size=n))
+    oc, c = _cache(orc, rng, dtype, H, D, bs, lens)
+    ids = rng.permutation(n).astype(np.int32)
+    if dup:
+        ids[dup[1]] = ids[dup[0]]
+    K, V, q = _inputs(rng, dtype, n, H, Hq, D)
+    say("decode step n", n, "repeated id at", dup)
+    if dup:
+        snap = _snapshot(c)
+        st_d, ref = oc.decode_attention(ids, wl.to_f64(q), Hq, D ** -0.5)
+        st_a = oc.append(ids, np.arange(n + 1, dtype=np.int32), wl.to_raw(K), wl.to_raw(V))
+        assert ERR_OF_STATUS[st_a] == sm.ERR_EINVAL
+        out, ws = _gpu_step(c, ids, K, V, q, 80)
+        _assert_unchanged(c, snap)
+        assert c.error_bits() == sm.ERR_EINVAL
+    else:
+        st_a, st_d, ref = _oracle_step(orc, oc, ids, K, V, q, Hq)
+        assert st_a == orc.OK
+        out, ws = _gpu_step(c, ids, K, V, q, 80)
+        assert c.error_bits() == 0
+        assert_same_state(c, oc)
+    _counters_clear(ws)
+    assert rel_l2_max(out.float().numpy(), ref) <= TOL[dtype]
