@@ -78,6 +78,8 @@ def _declare(L):
     L.orc_decode_attention.argtypes = [C.POINTER(_Cache), _P, _I, _P, _I, _D,
                                        _P, _P, _I]
     L.orc_decode_attention.restype = _I
+    L.orc_prefill_attention.argtypes = [C.POINTER(_Cache), _P, _I, _P, _P, _I, _D, _P]
+    L.orc_prefill_attention.restype = _I
     L.orc_layer_qkv.argtypes = [_I, _I, _P, _P, _I, _I, _I, _D, _D, _P, _P,
                                 _P, _P, _P, _P]
     L.orc_layer_qkv.restype = None
@@ -230,6 +232,17 @@ class OracleCache:
                                         num_q_heads, scale, _ptr(out), _ptr(probs), stride)
         if return_probs:
             return st, out, probs
+        return st, out
+
+    def prefill_attention(self, seq_ids, q_offsets, q, num_q_heads, scale):
+        """Causal attention of each request's last m_i cached positions;
+        q [rows, Hq, D] (any float), returns (status, out [rows, Hq, D])."""
+        seq_ids, q_offsets = _i32(seq_ids), _i32(q_offsets)
+        q = _f64(q)
+        out = np.zeros(q.shape)
+        s = self._struct()
+        st = lib().orc_prefill_attention(C.byref(s), _ptr(seq_ids), seq_ids.shape[0],
+                                         _ptr(q_offsets), _ptr(q), num_q_heads, scale, _ptr(out))
         return st, out
 
     # logical view helpers (pure indexing, used by tests)

@@ -25,6 +25,9 @@
  *     workloads), grouped-query head g = h / (Hq / Hkv), no soft-cap, no
  *     window; the query attends over every cached entry (it has been
  *     appended first).
+ *   - Prefill attention: the same scores, causal over cache positions; a
+ *     request's query rows are its last m cached positions (the prompt's
+ *     K/V are appended before the pass).
  */
 #include "oracle.h"
 
@@ -428,6 +431,73 @@ int orc_decode_attention(const orc_cache *c, const int32_t *seq_ids, int n,
     }
   }
   return status;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Prefill attention over the cache ("Efficiency Analysis": prompt merging  */
+/* shortens the sequence before the backbone runs, so every layer's         */
+/* attention runs over the compressed positions).  Causal: the query at     */
+/* cache position p sees entries 0..p.                                      */
+
+int orc_prefill_attention(const orc_cache *c, const int32_t *seq_ids, int n,
+                          const int32_t *q_offsets, const double *q,
+                          int num_q_heads, double scale, double *out) {
+  const int H = c->num_kv_heads, D = c->head_dim, bs = c->block_size;
+  if (n < 0 || num_q_heads <= 0 || num_q_heads % H != 0) return ORC_EINVAL;
+  if (n > 0 && q_offsets[0] != 0) return ORC_EINVAL;
+  for (int i = 0; i < n; ++i) {
+    const int s = seq_ids[i];
+    if (s < 0 || s >= c->max_seqs) return ORC_EINVAL;
+    const int32_t L = c->lengths[s];
+    const int32_t m = q_offsets[i + 1] - q_offsets[i];
+    if (L < 0 || L > (int64_t)c->max_blocks_per_seq * bs || m < 0 || m > L) return ORC_EINVAL;
+    const int32_t *row = c->block_table + (int64_t)s * c->max_blocks_per_seq;
+    for (int j = 0; j < L; j += bs)
+      if (row[j / bs] < 0 || row[j / bs] >= c->num_blocks) return ORC_EINVAL;
+  }
+  const int G = num_q_heads / H;
+  const int64_t rows = n > 0 ? q_offsets[n] : 0;
+  for (int64_t e = 0; e < rows * num_q_heads * D; ++e) out[e] = 0.0;
+
+  for (int i = 0; i < n; ++i) {
+    const int s = seq_ids[i];
+    const int32_t L = c->lengths[s];
+    const int32_t m = q_offsets[i + 1] - q_offsets[i];
+    const int32_t *row = c->block_table + (int64_t)s * c->max_blocks_per_seq;
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int r = 0; r < m; ++r) {
+      for (int hq = 0; hq < num_q_heads; ++hq) {
+        const int p = L - m + r;  /* this query's position */
+        const int g = hq / G;
+        const int64_t qi = ((int64_t)(q_offsets[i] + r) * num_q_heads + hq) * D;
+        const double *qv = q + qi;
+        double *o = out + qi;
+        double *sc = (double *)malloc(sizeof(double) * (size_t)(p + 1));
+        double mx = -INFINITY;
+        for (int j = 0; j <= p; ++j) {
+          const int blk = row[j / bs], slot = j % bs;
+          double dot = 0.0;
+          for (int t = 0; t < D; ++t)
+            dot += qv[t] * load_elem(c->k_pool, k_index(c, blk, g, slot, t), c->is_bf16);
+          sc[j] = dot * scale;
+          if (sc[j] > mx) mx = sc[j];
+        }
+        double Z = 0.0;
+        for (int j = 0; j <= p; ++j) {
+          sc[j] = exp(sc[j] - mx);
+          Z += sc[j];
+        }
+        for (int j = 0; j <= p; ++j) {
+          const int blk = row[j / bs], slot = j % bs;
+          const double w = sc[j] / Z;
+          for (int t = 0; t < D; ++t)
+            o[t] += w * load_elem(c->v_pool, v_index(c, blk, g, slot, t), c->is_bf16);
+        }
+        free(sc);
+      }
+    }
+  }
+  return ORC_OK;
 }
 
 /* ------------------------------------------------------------------------ */

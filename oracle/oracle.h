@@ -72,6 +72,16 @@ int orc_decode_attention(const orc_cache *c, const int32_t *seq_ids, int n,
                          double *out, double *probs /* nullable, see .c */,
                          int probs_stride);
 
+/* Prefill attention over the cache ("Efficiency Analysis": the prefill
+ * pass runs over the compressed sequence).  Request i's m_i query rows
+ * q[q_offsets[i] .. q_offsets[i+1]) are the last m_i cached positions of
+ * sequence seq_ids[i] (full prefill: m_i = length; chunked: fewer); row r
+ * sits at position p = L - m_i + r and attends causally to entries 0..p.
+ * q: [rows][num_q_heads][head_dim]; out: same shape. */
+int orc_prefill_attention(const orc_cache *c, const int32_t *seq_ids, int n,
+                          const int32_t *q_offsets, const double *q,
+                          int num_q_heads, double scale, double *out);
+
 /* Test-only attention-layer input side (not part of the merged path): unit
  * RMSNorm, then q/k/v projections, rotate-half RoPE at the given positions. */
 void orc_layer_qkv(int T, int d, const double *x, const int32_t *pos,
