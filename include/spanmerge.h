@@ -18,6 +18,9 @@
  *   sm_kv_rollback      crop k entries from the tail of each listed sequence
  *   sm_kv_append        append K/V rows (one surrogate state, or a prompt)
  *   sm_decode_attention one query per sequence over its whole paged cache
+ *   sm_prefill_attention causal attention of a prompt's positions over the
+ *                       paged cache (the prefill pass over the compressed
+ *                       sequence)
  *
  * General rules for every call
  * ----------------------------
@@ -312,6 +315,37 @@ sm_status sm_decode_step(const sm_paged_cache *c, const int32_t *seq_ids,
                          int n, const void *K, const void *V, const void *q,
                          int num_q_heads, float scale, int max_len, void *out,
                          void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * sm_prefill_attention -- the attention of the prefill pass over the
+ * compressed prompt ("Efficiency Analysis": prompt merging shortens the
+ * sequence before the backbone runs, so every layer attends over the
+ * compressed positions).  Request i's m_i = q_offsets[i+1] - q_offsets[i]
+ * query rows are the last m_i cached positions of sequence s = seq_ids[i]
+ * (append the prompt's K/V with sm_kv_append first; m_i < length gives a
+ * chunked prefill over earlier context).  Row r sits at position
+ * p = L - m_i + r, L = lengths[s], and attends causally to entries 0..p:
+ *
+ *   out[q_offsets[i] + r, h] = sum_{j <= p} softmax_j(scale q . K[s, j, g]) V[s, j, g]
+ *   g = h / (num_q_heads / num_kv_heads)
+ *
+ *  seq_ids      [n] ids in [0, max_seqs) (repeats allowed), n <= 65535
+ *  q_offsets    [n+1] row ranges into q and out, 0 <= q_offsets[i] <=
+ *               q_offsets[i+1] <= total_rows
+ *  total_rows   (host) rows of q and out
+ *  q            [total_rows][num_q_heads][head_dim], bf16
+ *  num_q_heads  (host) multiple of num_kv_heads, group size <= 16
+ *  max_rows     (host) upper bound on every m_i; sizes the grid
+ *  out          [total_rows][num_q_heads][head_dim], bf16
+ * bf16 caches only, head_dim 64 or 128, block_size a power of two >= 16,
+ * max_blocks_per_seq <= 4096.  No workspace.
+ * Device errors (into c->err; the request's rows are zero): EINVAL (bad id,
+ * bad row range, m_i > L or > max_rows, block id out of range).
+ */
+sm_status sm_prefill_attention(const sm_paged_cache *c, const int32_t *seq_ids,
+                               int n, const int32_t *q_offsets, int total_rows,
+                               const void *q, int num_q_heads, float scale,
+                               int max_rows, void *out, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -25,7 +25,8 @@ _P, _I, _L, _F, _Z = C.c_void_p, C.c_int, C.c_int64, C.c_float, C.c_size_t
 
 EXPORTED = ("sm_status_string", "sm_merge_workspace_bytes", "sm_merge_spans",
             "sm_pack_spans", "sm_kv_rollback", "sm_kv_append",
-            "sm_decode_workspace_bytes", "sm_decode_attention", "sm_decode_step")
+            "sm_decode_workspace_bytes", "sm_decode_attention", "sm_decode_step",
+            "sm_prefill_attention")
 
 
 class MergeParams(C.Structure):
@@ -80,6 +81,8 @@ def load(path: str = LIB_PATH):
     L.sm_decode_step.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _P, _P, _I, _F,
                                  _I, _P, _P, _Z, _P]
     L.sm_decode_step.restype = _I
+    L.sm_prefill_attention.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _I, _P, _I, _F, _I, _P, _P]
+    L.sm_prefill_attention.restype = _I
     _lib = L
     return L
 
@@ -227,3 +230,14 @@ def decode_step(cache: PagedCache, seq_ids, K, V, q, out, ws, max_len: int,
                                max_len, _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
                                _stream(stream))
     _check(st, "sm_decode_step")
+
+
+def prefill_attention(cache: PagedCache, seq_ids, q_offsets, q, out, max_rows: int,
+                      scale: Optional[float] = None, stream=None):
+    """Causal attention of each request's last m_i cached positions:
+    q, out [rows, Hq, D] bf16; q_offsets [n + 1] int32 row ranges."""
+    rows, Hq, D = q.shape
+    sc = D ** -0.5 if scale is None else scale
+    st = load().sm_prefill_attention(C.byref(cache.desc), _ptr(seq_ids), seq_ids.numel(), _ptr(q_offsets), rows,
+                                     _ptr(q), Hq, sc, max_rows, _ptr(out), _stream(stream))
+    _check(st, "sm_prefill_attention")

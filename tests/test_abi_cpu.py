@@ -66,6 +66,25 @@ def test_cache_descriptor_checks(L, kw):
     assert L.sm_kv_append(C.byref(d), 1, 1, 1, 1, 1, 1, None) == sm.SM_EINVAL
     assert L.sm_decode_attention(C.byref(d), 1, 1, 1, 8, 1.0, 16, 1, 1, 1 << 30, None) == sm.SM_EINVAL
     assert L.sm_decode_step(C.byref(d), 1, 1, 1, 1, 1, 8, 1.0, 16, 1, 1, 1 << 30, None) == sm.SM_EINVAL
+    assert L.sm_prefill_attention(C.byref(d), 1, 1, 1, 16, 1, 8, 1.0, 16, 1, None) == sm.SM_EINVAL
+
+
+def test_prefill_argument_checks(L):
+    d = _desc()
+    pf = lambda d, n=1, rows=16, hq=32, max_rows=16: L.sm_prefill_attention(C.byref(d), 1, n, 1, rows, 1, hq, 1.0,
+                                                                           max_rows, 1, None)
+    assert pf(d, n=0) == sm.SM_OK                         # nothing to do
+    assert pf(d, n=-1) == sm.SM_EINVAL
+    assert pf(d, rows=-1) == sm.SM_EINVAL
+    assert pf(d, max_rows=-1) == sm.SM_EINVAL
+    assert pf(d, hq=12) == sm.SM_EINVAL                   # Hq % Hkv
+    assert pf(d, hq=8 * 17) == sm.SM_EINVAL               # group > 16
+    assert pf(_desc(dtype=sm.SM_F32)) == sm.SM_EINVAL     # bf16 only
+    assert pf(_desc(head_dim=32)) == sm.SM_EINVAL
+    assert pf(_desc(max_blocks_per_seq=4097)) == sm.SM_EINVAL
+    assert L.sm_prefill_attention(C.byref(d), None, 1, 1, 16, 1, 32, 1.0, 16, 1, None) == sm.SM_EINVAL
+    assert L.sm_prefill_attention(C.byref(d), 1, 1, None, 16, 1, 32, 1.0, 16, 1, None) == sm.SM_EINVAL
+    assert L.sm_prefill_attention(C.byref(d), 1, 1, 1, 16, 1, 32, 1.0, 16, None, None) == sm.SM_EINVAL
 
 
 def test_request_count_and_workspace_checks(L):
