@@ -335,10 +335,12 @@ sm_status sm_decode_step(const sm_paged_cache *c, const int32_t *seq_ids,
  *  total_rows   (host) rows of q and out
  *  q            [total_rows][num_q_heads][head_dim], bf16
  *  num_q_heads  (host) multiple of num_kv_heads, group size <= 16
+ *  scale        (host) any finite value; 0 gives the mean of V[s, 0..p]
  *  max_rows     (host) upper bound on every m_i; sizes the grid
  *  out          [total_rows][num_q_heads][head_dim], bf16
  * bf16 caches only, head_dim 64 or 128, block_size a power of two >= 16,
- * max_blocks_per_seq <= 4096.  No workspace.
+ * max_blocks_per_seq <= 4096, one page of all kv heads (num_kv_heads x
+ * block_size x head_dim x 2 bytes) < 4 GiB.  No workspace.
  * Device errors (into c->err; the request's rows are zero): EINVAL (bad id,
  * bad row range, m_i > L or > max_rows, block id out of range).
  */

@@ -7,28 +7,44 @@
 //   out[row, h] = sum_{j <= p} softmax_j(scale q . K[s, j, g]) V[s, j, g],
 //   g = h / G (grouped query).
 //
-// One workgroup of four waves per (request, kv head, block of positions).
+// One workgroup of eight waves per (request, kv head, block of positions).
 // It holds 256 query vectors: BQ = 256 / G positions x the G query heads of
-// kv head g, so every K/V tile it loads serves all of them.  A wave owns 64
-// vectors as two 32-column blocks of the transposed score tile
+// kv head g, so every K/V tile it loads serves all of them.  A wave owns 32
+// vectors, the columns of the transposed score blocks
 //   S^T (32 keys x 32 queries) = K (32 x D) . Q^T        (v_mfma_f32_32x32x16_bf16)
 // and accumulates
 //   O^T (D x 32 queries) += V^T (D x 32 keys) . P^T.
+// At about 220 registers a wave, two waves share each SIMD, so one wave's
+// softmax runs while the other's products occupy the matrix unit.
 // In S^T a lane holds 16 keys of one query column, so the softmax row
-// statistics need one lane swap per tile.  The K rows of a tile are read in
+// statistics need one lane swap per tile.  The K rows of a block are read in
 // a permuted order so that the 16 scores a lane holds are exactly the keys
 // its PV operand needs (8 contiguous tokens per 16-key step): no shuffle
-// between the two products.  K/V tiles of 32 keys go through LDS, the next
+// between the two products.  K/V tiles of 64 keys go through LDS, the next
 // tile's global loads in flight while the current one is multiplied.
+//
+// Softmax: exp2 of (score x scale log2 e - reference), with the reference
+// (a running maximum) moved only when a tile's maximum exceeds it by more
+// than 2^8.  Any reference gives the same ratios; keeping it mostly fixed
+// skips the rescale of the accumulators on almost every tile.
 #include "common.hpp"
 
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// round-to-nearest-even pair conversion (one v_cvt_pk_bf16_f32 on gfx950)
+__device__ __forceinline__ uint32_t cvt_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
+}
 
 namespace sm {
 
-constexpr int kPfThreads = 256;
-constexpr int kPfVec = 256;   // query vectors per workgroup
-constexpr int kPfKeys = 32;   // keys per tile
+constexpr int kPfVec = 256;                 // query vectors per workgroup
+constexpr int kPfWaves = kPfVec / 32;       // one 32-vector column block per wave
+constexpr int kPfThreads = 64 * kPfWaves;
+constexpr int kPfKeys = 64;                 // keys per tile
+constexpr int kPfSub = kPfKeys / 32;        // 32-key score blocks per tile
 constexpr int kPfMaxPages = 4096;
 constexpr float kPfLog2e = 1.4426950408889634f;
 
@@ -42,11 +58,13 @@ struct PrefillArgs {
   const uint16_t *q;
   uint16_t *out;
   int32_t *err;
-  int n, total_rows, max_rows, Hkv, Hq, G, BQ, bs_log2, num_blocks, max_seqs, max_blocks;
-  float scale_log2e;
+  int n, total_rows, max_rows, Hkv, Hq, G, BQ, nqb, bs_log2, num_blocks, max_seqs, max_blocks;
+  uint32_t page_bytes;  // bytes of one page over all kv heads
+  float scale_log2e;    // |scale| log2(e), at least 1e-30
+  uint32_t q_sign;      // 0x80008000 when scale < 0: q enters with its sign flipped
 };
 
-// Score-tile row rho (0..31) holds token tau(rho) of the tile: within each
+// Score-block row rho (0..31) holds token tau(rho) of the block: within each
 // 16 rows the middle two groups of four swap places, so that the rows a lane
 // holds after S^T = K . Q^T ({8 g + 4 h + e}) are tokens 8 h .. 8 h + 7 of
 // each 16-key step, in register order.
@@ -57,22 +75,38 @@ __device__ __forceinline__ int pf_token_of_row(int rho) {
 }
 
 template <int DH>
-__global__ __launch_bounds__(kPfThreads, 1) void prefill_bf16(PrefillArgs a) {
+__global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16(PrefillArgs a) {
   constexpr int KP = DH + 8;        // K tile row pitch (bf16)
   constexpr int VP = kPfKeys + 8;   // V tile row pitch (bf16)
   constexpr int NKS = DH / 16;      // k steps of S^T
   constexpr int NRB = DH / 32;      // 32-dim row blocks of O^T
   constexpr int KCH = DH / 8;       // 16-byte chunks of a K row
-  constexpr int KU = kPfKeys * KCH / kPfThreads;  // K chunks per thread and tile
-  constexpr int VU = DH * (kPfKeys / 8) / kPfThreads;  // V chunks per thread and tile
-  static_assert(KU * kPfThreads == kPfKeys * KCH && VU * kPfThreads == DH * (kPfKeys / 8), "tile split");
+  constexpr int VCH = kPfKeys / 8;  // 16-byte chunks of a V row (one dim) in a tile
+  constexpr int KTOT = kPfKeys * KCH, VTOT = DH * VCH;    // 16-byte chunks per tile
+  constexpr int KU = (KTOT + kPfThreads - 1) / kPfThreads;  // K chunks per thread and tile
+  constexpr int VU = (VTOT + kPfThreads - 1) / kPfThreads;  // V chunks per thread and tile
   __shared__ int pages[kPfMaxPages];
   __shared__ int bad_flag;
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kPfKeys * KP];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][DH * VP];
 
-  const int qb = gridDim.x - 1 - blockIdx.x;  // longest blocks first
-  const int g = blockIdx.y, i = blockIdx.z;
+  // Workgroup -> (request i, kv head g, block qb).  Workgroups are dealt to
+  // the eight XCDs in turn; here the blocks of one (request, head) pair all
+  // land on one XCD, so its L2 fetches the pair's K/V once, and eight pairs
+  // run side by side.  Within a pair the longest blocks go first.
+  const int nqb = a.nqb, P = a.n * a.Hkv, Pfull = P & ~7;
+  const int b = blockIdx.x;
+  int pair, j;
+  if (b < Pfull * nqb) {
+    const int k = b >> 3;
+    pair = (k / nqb) * 8 + (b & 7);
+    j = k - (k / nqb) * nqb;
+  } else {
+    const int b2 = b - Pfull * nqb;
+    pair = Pfull + b2 / nqb;
+    j = b2 - (b2 / nqb) * nqb;
+  }
+  const int qb = nqb - 1 - j, g = pair % a.Hkv, i = pair / a.Hkv;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int c32 = lane & 31, h2 = lane >> 5;
   const int bs_log2 = a.bs_log2, bs = 1 << bs_log2;
@@ -127,84 +161,97 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_bf16(PrefillArgs a) {
     return;
   }
 
-  // ---- this wave's 64 query vectors: v = 64 w + 32 cb + c32 ----
-  // vector v -> query head g G + v / BQ, row q_lo + v % BQ
-  int vpos[2], vrow[2], vhead[2];
-  bool vok[2];
-  u32x4_t qf[2][NKS];
-#pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
-    const int v = 64 * w + 32 * cb + c32;
-    const int hh = v / a.BQ, rr = v - hh * a.BQ;
-    vok[cb] = hh < a.G && rr < nq;
-    vhead[cb] = g * a.G + (vok[cb] ? hh : 0);
-    vrow[cb] = r0 + q_lo + (vok[cb] ? rr : 0);
-    vpos[cb] = vok[cb] ? pos0 + rr : -1;  // an idle vector sees no key
-    const uint16_t *qp = a.q + ((int64_t)vrow[cb] * a.Hq + vhead[cb]) * DH + 8 * h2;
+  // ---- this wave's 32 query vectors: v = 32 w + c32 -> query head g G + v / BQ, row q_lo + v % BQ ----
+  const int v = 32 * w + c32;
+  const int hh = v / a.BQ, rr = v - hh * a.BQ;
+  const bool vok = hh < a.G && rr < nq;
+  const int vhead = g * a.G + (vok ? hh : 0);
+  const int vrow = r0 + q_lo + (vok ? rr : 0);
+  const int vpos = vok ? pos0 + rr : -1;  // an idle vector sees no key
+  u32x4_t qf[NKS];
+  {
+    const uint16_t *qp = a.q + ((int64_t)vrow * a.Hq + vhead) * DH + 8 * h2;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks)
-      qf[cb][ks] = vok[cb] ? *(const u32x4_t *)(qp + 16 * ks) : u32x4_t{0u, 0u, 0u, 0u};
+      qf[ks] = vok ? *(const u32x4_t *)(qp + 16 * ks) ^ a.q_sign : u32x4_t{0u, 0u, 0u, 0u};
   }
+  // wave-wide position range of the valid vectors: tiles past all of them
+  // are skipped, tiles before all of them need no mask
+  int wave_lo = vok ? vpos : 0x7fffffff, wave_hi = vpos;
+#pragma unroll
+  for (int sh = 1; sh < 64; sh <<= 1) {
+    wave_lo = min(wave_lo, __shfl_xor(wave_lo, sh));
+    wave_hi = max(wave_hi, __shfl_xor(wave_hi, sh));
+  }
+  wave_lo = __builtin_amdgcn_readfirstlane(wave_lo);
+  wave_hi = __builtin_amdgcn_readfirstlane(wave_hi);
 
-  // ---- tile loader: 2 K chunks and 2 V chunks of 16 bytes per thread ----
-  const int64_t page_elems = (int64_t)bs * DH;
+  // ---- tile loader: 16-byte chunks, K as rows of tokens, V as dim-major runs of 8 tokens ----
+  // A chunk's offset within its page is fixed per thread; a tile adds a
+  // uniform (t0 mod bs) and its page id.  Tokens past kend re-read page 0.
+  const uint64_t page_bytes = a.page_bytes;
+  const char *kbase = (const char *)a.k_pool + (int64_t)g * bs * DH * 2;
+  const char *vbase = (const char *)a.v_pool + (int64_t)g * bs * DH * 2;
+  int ktk[KU], koff[KU], vtk[VU], voff[VU];
+#pragma unroll
+  for (int u = 0; u < KU; ++u) {
+    const int id = min(tid + kPfThreads * u, KTOT - 1);
+    ktk[u] = id / KCH;
+    koff[u] = ((ktk[u] & (bs - 1)) * DH + (id % KCH) * 8) * 2;
+  }
+#pragma unroll
+  for (int u = 0; u < VU; ++u) {
+    const int id = min(tid + kPfThreads * u, VTOT - 1);
+    vtk[u] = 8 * (id % VCH);
+    voff[u] = ((id / VCH) * bs + (vtk[u] & (bs - 1))) * 2;
+  }
   auto fetch = [&](int t0, u32x4_t (&kv)[KU + VU]) {
+    const int tin = t0 & (bs - 1);  // 0 when a page is no longer than a tile
 #pragma unroll
     for (int u = 0; u < KU; ++u) {
-      const int id = tid + kPfThreads * u;
-      // K: token id / KCH, 8 dims (id % KCH); tokens past kend re-read token 0
-      int tok = t0 + id / KCH;
-      if (tok >= kend) tok = 0;
-      const int blk = pages[tok >> bs_log2];
-      kv[u] = *(const u32x4_t *)(a.k_pool + ((int64_t)blk * a.Hkv + g) * page_elems +
-                                 (int64_t)(tok & (bs - 1)) * DH + (id % KCH) * 8);
+      const int tok = t0 + ktk[u];
+      const uint32_t blk = pages[tok < kend ? tok >> bs_log2 : 0];
+      kv[u] = *(const u32x4_t *)(kbase + blk * page_bytes + (koff[u] + tin * DH * 2));
     }
 #pragma unroll
     for (int u = 0; u < VU; ++u) {
-      const int id = tid + kPfThreads * u;
-      // V: dim id / 4, tokens 8 (id % 4) .. + 7 (one page: bs >= 8)
-      const int d = id >> 2;
-      int tok = t0 + 8 * (id & 3);
-      const int nvalid = min(8, L - tok);  // entries past the length may hold anything
-      if (tok >= kend) tok = 0;
-      const int blk = pages[tok >> bs_log2];
-      u32x4_t x = *(const u32x4_t *)(a.v_pool + ((int64_t)blk * a.Hkv + g) * page_elems + (int64_t)d * bs +
-                                     (tok & (bs - 1)));
-      if (nvalid < 8) {
+      const int tok = t0 + vtk[u];
+      const uint32_t blk = pages[tok < kend ? tok >> bs_log2 : 0];
+      kv[KU + u] = *(const u32x4_t *)(vbase + blk * page_bytes + (voff[u] + tin * 2));
+    }
+    if (t0 + kPfKeys > L) {  // the last tile: V entries past the length may hold anything
+#pragma unroll
+      for (int u = 0; u < VU; ++u) {
+        const int nvalid = L - (t0 + vtk[u]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          if (2 * e >= nvalid) x[e] = 0u;
-          else if (2 * e + 1 >= nvalid) x[e] &= 0xffffu;
+          if (2 * e >= nvalid) kv[KU + u][e] = 0u;
+          else if (2 * e + 1 >= nvalid) kv[KU + u][e] &= 0xffffu;
         }
       }
-      kv[KU + u] = x;
     }
   };
   auto stash = [&](int buf, const u32x4_t (&kv)[KU + VU]) {
 #pragma unroll
     for (int u = 0; u < KU; ++u) {
       const int id = tid + kPfThreads * u;
-      *(u32x4_t *)(&k_lds[buf][(id / KCH) * KP + (id % KCH) * 8]) = kv[u];
+      if (KTOT % kPfThreads == 0 || id < KTOT) *(u32x4_t *)(&k_lds[buf][(id / KCH) * KP + (id % KCH) * 8]) = kv[u];
     }
 #pragma unroll
     for (int u = 0; u < VU; ++u) {
       const int id = tid + kPfThreads * u;
-      *(u32x4_t *)(&v_lds[buf][(id >> 2) * VP + 8 * (id & 3)]) = kv[KU + u];
+      if (VTOT % kPfThreads == 0 || id < VTOT) *(u32x4_t *)(&v_lds[buf][(id / VCH) * VP + 8 * (id % VCH)]) = kv[KU + u];
     }
   };
 
-  f32x16_t o[2][NRB];
+  f32x16_t o[NRB];
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb)
+  for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[cb][rb][e] = 0.f;
-  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+    for (int e = 0; e < 16; ++e) o[rb][e] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
   const float sl2 = a.scale_log2e;
   const int krow = pf_token_of_row(c32);  // this lane's K row in the S^T operand
-  // every vector of the workgroup sees key t when t <= pos0: no mask below
-  const int vpos_min = pos0;
 
   const int ntiles = (kend + kPfKeys - 1) / kPfKeys;
   u32x4_t stage[KU + VU];
@@ -215,92 +262,114 @@ __global__ __launch_bounds__(kPfThreads, 1) void prefill_bf16(PrefillArgs a) {
     const int buf = t & 1, t0 = t * kPfKeys;
     if (t + 1 < ntiles) fetch(t0 + kPfKeys, stage);  // in flight during this tile
 
-    // S^T = K . Q^T for both column blocks
-    const uint16_t *kl = &k_lds[buf][krow * KP + 8 * h2];
-    f32x16_t sc[2];
+    if (t0 <= wave_hi) {
+      // S^T = K . Q^T, one 32-key block at a time: its fragment reads first, then its products
+      f32x16_t sc[kPfSub];
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb)
+      for (int sb = 0; sb < kPfSub; ++sb) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sc[cb][e] = 0.f;
+        for (int e = 0; e < 16; ++e) sc[sb][e] = 0.f;
+        const uint16_t *kl = &k_lds[buf][(32 * sb + krow) * KP + 8 * h2];
+        u32x4_t kf[NKS];
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      const u32x4_t kf = *(const u32x4_t *)(kl + 16 * ks);
+        for (int ks = 0; ks < NKS; ++ks) kf[ks] = *(const u32x4_t *)(kl + 16 * ks);
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb)
-        sc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf), as_bf16x8(qf[cb][ks]), sc[cb], 0, 0, 0);
-    }
+        for (int ks = 0; ks < NKS; ++ks)
+          sc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[ks]), as_bf16x8(qf[ks]), sc[sb], 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, NKS, 0);  // LDS reads
+        __builtin_amdgcn_sched_group_barrier(0x008, NKS, 0);  // MFMA
+      }
+      // V fragments of the first block: lane (d, h2) feeds dims 32 rb + d, tokens 16 kst + 8 h2 .. +7
+      u32x4_t vf[NRB][2];
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int kst = 0; kst < 2; ++kst)
+          vf[rb][kst] = *(const u32x4_t *)(&v_lds[buf][(32 * rb + c32) * VP + 16 * kst + 8 * h2]);
 
-    // online softmax per query column; register 4 gg + e holds token
-    // t0 + 8 (gg >> 1) * 2 ... : row 8 gg + 4 h2 + e -> token pf_token_of_row(row)
-    const bool need_mask = t0 + kPfKeys - 1 > vpos_min;
-    u32x4_t pf[2][2];
+      // online softmax per query column; register r of block sb holds token
+      // t0 + 32 sb + tau(8 (r >> 2) + 4 h2 + (r & 3)).  Masked scores become
+      // -inf in place: exp2 of -inf is 0 (the multiplier is positive).
+      if (t0 + kPfKeys - 1 > wave_lo) {
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
-      float x[16];
+        for (int sb = 0; sb < kPfSub; ++sb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int tok = t0 + 32 * sb + pf_token_of_row(8 * (r >> 2) + 4 * h2 + (r & 3));
+            sc[sb][r] = tok <= vpos ? sc[sb][r] : -INFINITY;
+          }
+      }
       float mx = -INFINITY;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int tok = t0 + pf_token_of_row(8 * (r >> 2) + 4 * h2 + (r & 3));
-        const bool valid = !need_mask || tok <= vpos[cb];
-        x[r] = valid ? sc[cb][r] * sl2 : -INFINITY;
-        mx = fmaxf(mx, x[r]);
-      }
+      for (int sb = 0; sb < kPfSub; ++sb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[sb][r]);
       float a0, b0;
       swap32(mx, a0, b0);
       mx = fmaxf(a0, b0);
-      const float m_new = fmaxf(m_run[cb], mx);
+      const float ms = mx == -INFINITY ? -INFINITY : mx * sl2;  // in log2 units
+      const bool move = ms > m_run + 8.0f;
+      const float m_new = move ? ms : m_run;
       const float mb = m_new == -INFINITY ? 0.f : m_new;  // a column with no key yet
-      const float alpha = exp2f(m_run[cb] - mb);
+      if (__ballot(move) != 0) {  // rare: rescale before this tile's products are added
+        const float alpha = move ? __builtin_amdgcn_exp2f(m_run - mb) : 1.f;
+        l_run *= alpha;
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) o[rb] *= alpha;
+      }
+      m_run = m_new;
       float ps = 0.f;
+      u32x4_t pf[kPfSub][2];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        x[r] = exp2f(x[r] - mb);
-        ps += x[r];
+      for (int sb = 0; sb < kPfSub; ++sb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          sc[sb][r] = __builtin_amdgcn_exp2f(fmaf(sc[sb][r], sl2, -mb));
+          ps += sc[sb][r];
+        }
+        const f32x16_t &x = sc[sb];
+#pragma unroll
+        for (int kst = 0; kst < 2; ++kst)
+          pf[sb][kst] = u32x4_t{cvt_bf16x2(x[8 * kst + 0], x[8 * kst + 1]), cvt_bf16x2(x[8 * kst + 2], x[8 * kst + 3]),
+                                cvt_bf16x2(x[8 * kst + 4], x[8 * kst + 5]), cvt_bf16x2(x[8 * kst + 6], x[8 * kst + 7])};
       }
-      l_run[cb] = l_run[cb] * alpha + ps;
-      m_run[cb] = m_new;
-#pragma unroll
-      for (int rb = 0; rb < NRB; ++rb) o[cb][rb] *= alpha;
-#pragma unroll
-      for (int kst = 0; kst < 2; ++kst)
-        pf[cb][kst] = u32x4_t{pack_bf16x2(x[8 * kst + 0], x[8 * kst + 1]), pack_bf16x2(x[8 * kst + 2], x[8 * kst + 3]),
-                              pack_bf16x2(x[8 * kst + 4], x[8 * kst + 5]), pack_bf16x2(x[8 * kst + 6], x[8 * kst + 7])};
-    }
+      l_run += ps;
 
-    // O^T += V^T . P^T: lane (d, h2) feeds dims 32 rb + d, tokens 16 kst + 8 h2 .. +7
+      // O^T += V^T . P^T
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
+      for (int sb = 0; sb < kPfSub; ++sb) {
+        if (sb > 0) {
 #pragma unroll
-      for (int kst = 0; kst < 2; ++kst) {
-        const u32x4_t vf = *(const u32x4_t *)(&v_lds[buf][(32 * rb + c32) * VP + 16 * kst + 8 * h2]);
+          for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
-          o[cb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf), as_bf16x8(pf[cb][kst]), o[cb][rb], 0, 0, 0);
+            for (int kst = 0; kst < 2; ++kst)
+              vf[rb][kst] = *(const u32x4_t *)(&v_lds[buf][(32 * rb + c32) * VP + 32 * sb + 16 * kst + 8 * h2]);
+        }
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+          for (int kst = 0; kst < 2; ++kst)
+            o[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[rb][kst]), as_bf16x8(pf[sb][kst]), o[rb], 0, 0, 0);
       }
+    }
 
     if (t + 1 < ntiles) stash(buf ^ 1, stage);
     __syncthreads();
   }
 
   // ---- normalize and store: register 4 gg + e of block rb = dim 32 rb + 8 gg + 4 h2 + e ----
+  float a0, b0;
+  swap32(l_run, a0, b0);
+  const float l_tot = a0 + b0;
+  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+  if (!vok) return;
+  uint16_t *op = a.out + ((int64_t)vrow * a.Hq + vhead) * DH + 4 * h2;
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
-    float a0, b0;
-    swap32(l_run[cb], a0, b0);
-    const float l_tot = a0 + b0;
-    const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
-    if (!vok[cb]) continue;
-    uint16_t *op = a.out + ((int64_t)vrow[cb] * a.Hq + vhead[cb]) * DH + 4 * h2;
+  for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-      for (int gg = 0; gg < 4; ++gg) {
-        const f32x16_t &acc = o[cb][rb];
-        *(uint2 *)(op + 32 * rb + 8 * gg) =
-            make_uint2(pack_bf16x2(acc[4 * gg + 0] * inv, acc[4 * gg + 1] * inv),
-                       pack_bf16x2(acc[4 * gg + 2] * inv, acc[4 * gg + 3] * inv));
-      }
-  }
+    for (int gg = 0; gg < 4; ++gg)
+      *(uint2 *)(op + 32 * rb + 8 * gg) = make_uint2(cvt_bf16x2(o[rb][4 * gg + 0] * inv, o[rb][4 * gg + 1] * inv),
+                                                     cvt_bf16x2(o[rb][4 * gg + 2] * inv, o[rb][4 * gg + 3] * inv));
 }
 
 }  // namespace sm
@@ -315,7 +384,7 @@ SM_API sm_status sm_prefill_attention(const sm_paged_cache *c, const int32_t *se
   if (!seq_ids || !q_offsets || !q || !out || !c->k_pool || !c->v_pool || !c->block_table || !c->lengths ||
       !c->err)
     return SM_EINVAL;
-  if (c->dtype != SM_BF16) return SM_EINVAL;
+  if (c->dtype != SM_BF16 || !(fabsf(scale) <= 3.0e38f)) return SM_EINVAL;  // a finite scale
   const int H = c->num_kv_heads, D = c->head_dim, bs = c->block_size;
   if (H <= 0 || num_q_heads <= 0 || num_q_heads % H != 0) return SM_EINVAL;
   const int G = num_q_heads / H;
@@ -323,7 +392,7 @@ SM_API sm_status sm_prefill_attention(const sm_paged_cache *c, const int32_t *se
   if (bs < 16 || (bs & (bs - 1)) != 0 || c->max_blocks_per_seq <= 0 || c->max_blocks_per_seq > kPfMaxPages ||
       c->num_blocks <= 0 || c->max_seqs <= 0)
     return SM_EINVAL;
-  if (n > 65535) return SM_EINVAL;
+  if (n > 65535 || (uint64_t)H * bs * D * 2 > 0xffffffffull) return SM_EINVAL;
   PrefillArgs a;
   a.k_pool = (const uint16_t *)c->k_pool;
   a.v_pool = (const uint16_t *)c->v_pool;
@@ -347,10 +416,15 @@ SM_API sm_status sm_prefill_attention(const sm_paged_cache *c, const int32_t *se
   a.num_blocks = c->num_blocks;
   a.max_seqs = c->max_seqs;
   a.max_blocks = c->max_blocks_per_seq;
-  a.scale_log2e = scale * kPfLog2e;
+  a.page_bytes = (uint32_t)((uint64_t)H * bs * D * 2);
+  // A positive multiplier keeps exp2(-inf) = 0 for masked keys.  Below 1e-30
+  // every weight rounds to 1 in fp32 either way (|q . k| stays far below 1e30).
+  a.scale_log2e = fmaxf(fabsf(scale) * kPfLog2e, 1e-30f);
+  a.q_sign = scale < 0.f ? 0x80008000u : 0u;
   const int nqb = max_rows > 0 ? (max_rows + a.BQ - 1) / a.BQ : 1;  // block 0 reports bad requests
-  if (nqb > (1 << 30)) return SM_EINVAL;
-  const dim3 grid(nqb, H, n);
+  if ((int64_t)nqb * n * H > 0x7fffffff) return SM_EINVAL;
+  a.nqb = nqb;
+  const dim3 grid(nqb * n * H);
   if (D == 128)
     hipLaunchKernelGGL(prefill_bf16<128>, grid, dim3(kPfThreads), 0, stream, a);
   else

@@ -85,6 +85,10 @@ def test_prefill_argument_checks(L):
     assert L.sm_prefill_attention(C.byref(d), None, 1, 1, 16, 1, 32, 1.0, 16, 1, None) == sm.SM_EINVAL
     assert L.sm_prefill_attention(C.byref(d), 1, 1, None, 16, 1, 32, 1.0, 16, 1, None) == sm.SM_EINVAL
     assert L.sm_prefill_attention(C.byref(d), 1, 1, 1, 16, 1, 32, 1.0, 16, None, None) == sm.SM_EINVAL
+    for bad in (float("nan"), float("inf"), -float("inf")):                   # the scale must be finite
+        assert L.sm_prefill_attention(C.byref(d), 1, 1, 1, 16, 1, 32, bad, 16, 1, None) == sm.SM_EINVAL
+    # one page over all kv heads must stay below 4 GiB: 8 heads x 2^22 tokens x 128 dims x 2 bytes = 8 GiB
+    assert pf(_desc(block_size=1 << 22)) == sm.SM_EINVAL
 
 
 def test_request_count_and_workspace_checks(L):

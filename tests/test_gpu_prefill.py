@@ -43,6 +43,9 @@ CASES = [
     (16, 1, 64, 16, [150, 20, 0], [150, 3, 0]),                 # group of 16, head_dim 64, an empty request
     (8, 4, 64, 128, [400, 129], [400, 100]),
     (4, 2, 128, 512, [700], [513]),
+    (8, 2, 128, 32, [130, 64, 1], None),                        # two pages per 64-key tile
+    (8, 2, 128, 64, [200, 65], [200, 1]),                       # one page per tile
+    (12, 3, 64, 256, [300, 257], [300, 129]),                   # pages longer than a tile, D 64
 ]
 
 
@@ -62,6 +65,29 @@ def test_prefill_matches_oracle(orc, case):
     out = _gpu_prefill(c, ids, qo, q, max(ms))
     assert c.error_bits() == 0
     e = rel_l2_max(out, ref)
+    say("rel_l2_max", e)
+    assert e <= TOL[torch.bfloat16]
+
+
+@pytest.mark.parametrize("scale", [-0.09, 0.0, 0.4])
+def test_prefill_scale_values(orc, scale):
+    """Negative, zero (the plain mean of the visible V rows) and large scales."""
+    Hq, H, D, bs = 8, 2, 128, 16
+    rng = np.random.RandomState(31)
+    lens = [150, 70]
+    oc, c = _cache(orc, rng, H, D, bs, lens)
+    ids = np.arange(len(lens), dtype=np.int32)
+    qo = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    g = wl.generator(32)
+    q = wl.randn((int(qo[-1]), Hq, D), torch.bfloat16, g)
+    st, ref = oc.prefill_attention(ids, qo, wl.to_f64(q), Hq, scale)
+    assert st == orc.OK
+    say("prefill scale", scale)
+    out = torch.full(q.shape, float("nan"), dtype=torch.bfloat16, device=dev())
+    sm.prefill_attention(c, i32(ids), i32(qo), q.to(dev()), out, max(lens), scale=scale)
+    torch.cuda.synchronize()
+    assert c.error_bits() == 0
+    e = rel_l2_max(out.float().cpu().numpy(), ref)
     say("rel_l2_max", e)
     assert e <= TOL[torch.bfloat16]
 
