@@ -392,6 +392,7 @@ def extras_report(job, stream, attn_us):
     torch.cuda.empty_cache()
 
     out["merge_spans_70b_prompt_batch"] = merge_70b_report(job.sm, job.L, dev, stream)
+    out["prefill_attention"] = prefill_report(job.sm, job.L, dev, stream)
     return out
 
 
@@ -431,6 +432,51 @@ def merge_70b_report(sm, L, dev, stream, reps=3):
         "frac_of_bf16_peak": round(flop5 / (t5 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "note": "one sm_merge_spans call over every span of the 32 x 8192 prompts; FLOP = 2 d^2 (rows + spans) "
                 "for the two projections (pooling and LayerNorm are O(d) per row)"}
+
+
+def prefill_report(sm, L, dev, stream, reps=10):
+    """Prefill attention (one layer, all 32 query heads) over the 16-prompt
+    batch: the span-compacted prompts (2458 positions) against the same
+    batch uncompressed (4096).  FLOP = 4 Hq D sum over rows of (position + 1)
+    for the two causal products."""
+    import torch
+    from paper_2609_27233_amd import workload as wl
+    w = wl.WORKLOADS[2]
+    B, H, D, Hq, bs = w.batch, w.num_kv_heads, w.head_dim, w.num_q_heads, w.block_size
+    st = stream.cuda_stream
+    g = wl.generator(91, dev)
+    res = {}
+    for name, Lp in (("compacted", w.prompt_len - int(round(w.target * w.prompt_len))), ("uncompressed", w.prompt_len)):
+        nb = -(-Lp // bs)
+        c = sm.PagedCache(dtype=torch.bfloat16, num_kv_heads=H, head_dim=D, block_size=bs, num_blocks=B * nb,
+                          max_seqs=B, max_blocks_per_seq=nb, device=dev)
+        offs = torch.arange(B + 1, dtype=torch.int32, device=dev) * Lp
+        ids = torch.arange(B, dtype=torch.int32, device=dev)
+        K = wl.randn((B * Lp, H, D), torch.bfloat16, g, device=dev)
+        V = wl.randn((B * Lp, H, D), torch.bfloat16, g, device=dev)
+        sm.kv_append(c, ids, offs, K, V, stream=stream)
+        del K, V
+        q = wl.randn((B * Lp, Hq, D), torch.bfloat16, g, device=dev)
+        out = torch.empty_like(q)
+        d = C.byref(c.desc)
+
+        def call():
+            rc = L.sm_prefill_attention(d, ids.data_ptr(), B, offs.data_ptr(), B * Lp, q.data_ptr(), Hq,
+                                        D ** -0.5, Lp, out.data_ptr(), st)
+            if rc:
+                raise RuntimeError(f"sm_prefill_attention failed: {rc}")
+        t = _time(call, stream, reps)
+        assert c.error_bits() == 0
+        flop = 4.0 * Hq * D * B * Lp * (Lp + 1) / 2
+        res[name] = {"positions": Lp, "ms": round(t, 4), "TFLOPs": round(flop / (t * 1e-3) / 1e12, 1),
+                     "frac_of_bf16_peak": round(flop / (t * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        del c, q, out
+        torch.cuda.empty_cache()
+        log(f"extras: prefill attention over {Lp} positions done")
+    res["speedup"] = round(res["uncompressed"]["ms"] / res["compacted"]["ms"], 3)
+    res["kernel"] = "prefill_bf16<128>: causal grouped-query attention of 16 prompts x 32 heads over the paged cache"
+    res["note"] = "HIP events around back-to-back calls; one layer's attention, K/V already appended"
+    return res
 
 
 def traffic_bytes(alg_bytes):
@@ -525,6 +571,8 @@ def main():
                     help="only run a plain device copy of BYTES three times (scales HBM counters) and exit")
     ap.add_argument("--merge-only", action="store_true",
                     help="only time the merge module over the 70B-shaped prompt batch and print that")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="only time the prefill attention over the compacted and uncompressed prompt batch")
     ap.add_argument("--overlap", action="store_true",
                     help="run cache updates on a second stream, overlapped with other batches' attention")
     args = ap.parse_args()
@@ -550,6 +598,10 @@ def main():
     if args.merge_only:
         from paper_2609_27233_amd import lib as sm
         print(json.dumps(merge_70b_report(sm, sm.load(), dev, torch.cuda.current_stream(), reps=5)), flush=True)
+        return
+    if args.prefill_only:
+        from paper_2609_27233_amd import lib as sm
+        print(json.dumps(prefill_report(sm, sm.load(), dev, torch.cuda.current_stream())), flush=True)
         return
     w = wl.WORKLOADS[2]
     if args.decode_steps is not None:
