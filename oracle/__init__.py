@@ -64,6 +64,10 @@ class _Cache(C.Structure):
                 ("free_top", _P)]
 
 
+class _Rules(C.Structure):
+    _fields_ = [("count", _I), ("keys", _P), ("ids", _P)]
+
+
 def _declare(L):
     L.orc_merge_spans.argtypes = [_I, _I, _D, _P, _L, _P, _P, _I, _P, _P, _P,
                                   _P, _P, _P, _P, _P, _P, _I, _P, _P, _I]
@@ -83,6 +87,17 @@ def _declare(L):
     L.orc_layer_qkv.argtypes = [_I, _I, _P, _P, _I, _I, _I, _D, _D, _P, _P,
                                 _P, _P, _P, _P]
     L.orc_layer_qkv.restype = None
+    L.orc_rules_init.argtypes = [C.POINTER(_Rules), _P, _I]
+    L.orc_rules_init.restype = _I
+    L.orc_rules_free.argtypes = [C.POINTER(_Rules)]
+    L.orc_rules_free.restype = None
+    L.orc_rules_find.argtypes = [C.POINTER(_Rules), _P, _I]
+    L.orc_rules_find.restype = _I
+    L.orc_match_prompt.argtypes = [C.POINTER(_Rules), _I, _P, _P, _P, _P, _P, _P]
+    L.orc_match_prompt.restype = _I
+    L.orc_match_decode_step.argtypes = [C.POINTER(_Rules), _P, C.POINTER(_I), C.c_int32, C.POINTER(C.c_int32),
+                                        C.POINTER(C.c_int32)]
+    L.orc_match_decode_step.restype = None
     L.orc_num_threads.argtypes = []
     L.orc_num_threads.restype = _I
 
@@ -272,3 +287,72 @@ def layer_qkv(x, pos, W_q, W_k, W_v, num_q_heads, num_kv_heads, head_dim,
                         head_dim, rope_theta, rms_eps, _ptr(_f64(W_q)),
                         _ptr(_f64(W_k)), _ptr(_f64(W_v)), _ptr(q), _ptr(k), _ptr(v))
     return q, k, v
+
+
+# --------------------------------------------------------------------------
+# merge rules and matching
+
+MERGED = -2  # a surrogate in the decode-time generated-state list
+
+
+def rule_keys(grams):
+    """[m, 4] int32 keys of n-grams given as sequences (unused tail -1)."""
+    out = np.full((len(grams), 4), -1, dtype=np.int32)
+    for i, g in enumerate(grams):
+        out[i, :len(g)] = g
+    return out
+
+
+class OracleRules:
+    """The rule set R (sorted, searched by bisection) and the two matching
+    procedures of the appendix."""
+
+    def __init__(self, keys):
+        self.keys_in = _i32(np.asarray(keys).reshape(-1, 4))
+        self._r = _Rules()
+        self.status = lib().orc_rules_init(C.byref(self._r), _ptr(self.keys_in), self.keys_in.shape[0])
+        self._states = {}
+
+    def __del__(self):
+        try:
+            lib().orc_rules_free(C.byref(self._r))
+        except Exception:
+            pass
+
+    @property
+    def count(self):
+        return self._r.count
+
+    def find(self, gram):
+        g = _i32(gram)
+        return lib().orc_rules_find(C.byref(self._r), _ptr(g), g.shape[0])
+
+    def match_prompt(self, token_ids, seq_offsets):
+        """(status, span_start, span_len, span_rule, seq_span_offsets)."""
+        tok, so = _i32(token_ids), _i32(seq_offsets)
+        B = so.shape[0] - 1
+        cap = max(int(so[-1]) // 2, 1)
+        st_, ln, ru = (np.zeros(cap, np.int32) for _ in range(3))
+        sso = np.zeros(B + 1, np.int32)
+        st = lib().orc_match_prompt(C.byref(self._r), B, _ptr(so), _ptr(tok), _ptr(st_), _ptr(ln), _ptr(ru),
+                                    _ptr(sso))
+        S = int(sso[-1])
+        return st, st_[:S].copy(), ln[:S].copy(), ru[:S].copy(), sso
+
+    def decode_step(self, seq, token):
+        """Feed one generated token of sequence `seq`; returns (k, rule id)."""
+        buf, n = self._states.get(seq, (np.zeros(16, np.int32), 0))
+        if n + 1 > buf.shape[0]:
+            nb = np.zeros(2 * buf.shape[0], np.int32)
+            nb[:n] = buf[:n]
+            buf = nb
+        ln = C.c_int(n)
+        k, rule = C.c_int32(0), C.c_int32(-1)
+        lib().orc_match_decode_step(C.byref(self._r), _ptr(buf), C.byref(ln), int(token), C.byref(k),
+                                    C.byref(rule))
+        self._states[seq] = (buf, ln.value)
+        return k.value, rule.value
+
+    def state(self, seq):
+        buf, n = self._states.get(seq, (np.zeros(0, np.int32), 0))
+        return buf[:n].copy()

@@ -542,3 +542,134 @@ void orc_layer_qkv(int T, int d, const double *x, const int32_t *pos,
   }
   free(xn);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Merge rules and their matching (appendix "Non-overlapping Assignment in  */
+/* a Sequence", "Rule Matching", "Decoding-time Integration").              */
+
+static int key_cmp(const int32_t *a, const int32_t *b) {
+  for (int i = 0; i < 4; ++i)
+    if (a[i] != b[i]) return a[i] < b[i] ? -1 : 1;
+  return 0;
+}
+
+static int rule_len(const int32_t *k) { /* n >= 2 leading ids >= 0, then -1; else 0 */
+  int n = 0;
+  while (n < 4 && k[n] >= 0) ++n;
+  for (int i = n; i < 4; ++i)
+    if (k[i] != -1) return 0;
+  return n >= 2 ? n : 0;
+}
+
+static const int32_t *g_sort_keys; /* qsort context: input rules */
+static int idx_cmp(const void *pa, const void *pb) {
+  const int32_t a = *(const int32_t *)pa, b = *(const int32_t *)pb;
+  const int c = key_cmp(g_sort_keys + 4 * (int64_t)a, g_sort_keys + 4 * (int64_t)b);
+  return c != 0 ? c : (a < b ? -1 : a > b);
+}
+
+int orc_rules_init(orc_rules *r, const int32_t *rules, int count) {
+  r->count = 0;
+  r->keys = NULL;
+  r->ids = NULL;
+  if (count < 0) return ORC_EINVAL;
+  for (int i = 0; i < count; ++i)
+    if (!rule_len(rules + 4 * (int64_t)i)) return ORC_EINVAL;
+  int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)(count > 0 ? count : 1));
+  for (int i = 0; i < count; ++i) order[i] = i;
+  g_sort_keys = rules;
+  qsort(order, (size_t)count, sizeof(int32_t), idx_cmp);
+  r->keys = (int32_t *)malloc(sizeof(int32_t) * 4 * (size_t)(count > 0 ? count : 1));
+  r->ids = (int32_t *)malloc(sizeof(int32_t) * (size_t)(count > 0 ? count : 1));
+  for (int i = 0; i < count; ++i) {
+    const int32_t *k = rules + 4 * (int64_t)order[i];
+    /* equal keys are adjacent, smallest index first: keep that one */
+    if (r->count > 0 && key_cmp(r->keys + 4 * (int64_t)(r->count - 1), k) == 0) continue;
+    for (int j = 0; j < 4; ++j) r->keys[4 * (int64_t)r->count + j] = k[j];
+    r->ids[r->count++] = order[i];
+  }
+  free(order);
+  return ORC_OK;
+}
+
+void orc_rules_free(orc_rules *r) {
+  free(r->keys);
+  free(r->ids);
+  r->keys = NULL;
+  r->ids = NULL;
+  r->count = 0;
+}
+
+int orc_rules_find(const orc_rules *r, const int32_t *gram, int n) {
+  if (n < 2 || n > 4) return -1;
+  int32_t k[4] = {-1, -1, -1, -1};
+  for (int i = 0; i < n; ++i) {
+    if (gram[i] < 0) return -1;
+    k[i] = gram[i];
+  }
+  int lo = 0, hi = r->count - 1;
+  while (lo <= hi) {
+    const int mid = lo + (hi - lo) / 2;
+    const int c = key_cmp(r->keys + 4 * (int64_t)mid, k);
+    if (c == 0) return r->ids[mid];
+    if (c < 0) lo = mid + 1;
+    else hi = mid - 1;
+  }
+  return -1;
+}
+
+int orc_match_prompt(const orc_rules *r, int B, const int32_t *seq_offsets,
+                     const int32_t *token_ids, int32_t *span_start,
+                     int32_t *span_len, int32_t *span_rule,
+                     int32_t *seq_span_offsets) {
+  if (B < 0 || seq_offsets[0] != 0) return ORC_EINVAL;
+  for (int b = 0; b < B; ++b)
+    if (seq_offsets[b + 1] < seq_offsets[b]) return ORC_EINVAL;
+  int S = 0;
+  for (int b = 0; b < B; ++b) {
+    seq_span_offsets[b] = S;
+    const int32_t *x = token_ids + seq_offsets[b];
+    const int T = seq_offsets[b + 1] - seq_offsets[b];
+    int i = 0;
+    while (i < T) {
+      int taken = 0;
+      for (int n = 4; n >= 2 && !taken; --n) {
+        if (i + n > T) continue;
+        const int id = orc_rules_find(r, x + i, n);
+        if (id >= 0) {
+          span_start[S] = seq_offsets[b] + i;
+          span_len[S] = n;
+          span_rule[S] = id;
+          ++S;
+          i += n;
+          taken = 1;
+        }
+      }
+      if (!taken) i += 1;
+    }
+  }
+  seq_span_offsets[B] = S;
+  return ORC_OK;
+}
+
+void orc_match_decode_step(const orc_rules *r, int32_t *state, int *state_len,
+                           int32_t token, int32_t *k_out, int32_t *rule_out) {
+  state[(*state_len)++] = token;
+  *k_out = 0;
+  *rule_out = -1;
+  for (int n = 4; n >= 2; --n) {
+    if (*state_len < n) continue;
+    const int32_t *tail = state + *state_len - n;
+    int raw = 1;
+    for (int j = 0; j < n; ++j)
+      if (tail[j] == ORC_MERGED) raw = 0;
+    if (!raw) continue;
+    const int id = orc_rules_find(r, tail, n);
+    if (id < 0) continue;
+    *state_len -= n;
+    state[(*state_len)++] = ORC_MERGED;
+    *k_out = n - 1;
+    *rule_out = id;
+    return;
+  }
+}

@@ -90,6 +90,46 @@ void orc_layer_qkv(int T, int d, const double *x, const int32_t *pos,
                    const double *W_k, const double *W_v, double *q, double *k,
                    double *v);
 
+/* Merge rules (appendix "Non-overlapping Assignment in a Sequence" and
+ * "Rule Matching").  A rule is an n-gram of token ids, n = 2..4, given as 4
+ * int32 with the unused tail set to -1.  The rule set R is a set: a rule
+ * listed twice keeps its first index as its id.  The oracle holds R as a
+ * sorted array searched by bisection. */
+typedef struct {
+  int count;      /* distinct rules */
+  int32_t *keys;  /* [count][4], sorted lexicographically */
+  int32_t *ids;   /* [count] smallest input index of each key */
+} orc_rules;
+
+/* Validates every rule (n >= 2 leading ids >= 0, then -1) and builds R;
+ * EINVAL (and an empty set) if any rule is malformed. */
+int orc_rules_init(orc_rules *r, const int32_t *rules, int count);
+void orc_rules_free(orc_rules *r);
+/* id of the n-gram gram[0..n) in R, or -1 (any negative token: -1). */
+int orc_rules_find(const orc_rules *r, const int32_t *gram, int n);
+
+/* Prompt-time assignment: for each sequence b (tokens seq_offsets[b] ..
+ * seq_offsets[b+1]) scan left to right; at position i try n = 4, 3, 2 and
+ * take the first n whose full window is a rule, then jump past it, else
+ * step one token.  Spans come out in order: global start, length, rule id;
+ * seq_span_offsets [B+1] gives each sequence's range.  Capacity of the span
+ * arrays: seq_offsets[B] / 2. */
+int orc_match_prompt(const orc_rules *r, int B, const int32_t *seq_offsets,
+                     const int32_t *token_ids, int32_t *span_start,
+                     int32_t *span_len, int32_t *span_rule,
+                     int32_t *seq_span_offsets);
+
+/* Decode-time check after one generated token (appendix "Decoding-time
+ * Integration"): state[0..*state_len) is the generated-state list, raw
+ * token ids >= 0 and ORC_MERGED for a surrogate.  The token is appended,
+ * then the longest n in 4, 3, 2 whose last n entries are all raw and form a
+ * rule is merged: those n entries become one ORC_MERGED.  *k_out = n - 1
+ * entries to crop from the cache (0 without a match), *rule_out = rule id
+ * or -1.  The list needs room for one more entry. */
+#define ORC_MERGED (-2)
+void orc_match_decode_step(const orc_rules *r, int32_t *state, int *state_len,
+                           int32_t token, int32_t *k_out, int32_t *rule_out);
+
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int orc_num_threads(void);
 
