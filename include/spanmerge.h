@@ -10,7 +10,7 @@
  * rolls back the n-1 cached entries of a freshly completed span and appends
  * the surrogate's single K/V state (appendix "Inference with UMIM: Prompt and
  * Decoding-Time Merging").  Every later decode step then attends over the
- * shorter cache.  The five calls below are the device-side steps of that
+ * shorter cache.  The calls below are the device-side steps of that
  * path:
  *
  *   sm_merge_spans      z_s = M_phi(e(x_span))            for every span s
@@ -21,6 +21,11 @@
  *   sm_prefill_attention causal attention of a prompt's positions over the
  *                       paged cache (the prefill pass over the compressed
  *                       sequence)
+ *   sm_rules_build      the merge-rule set R as a device hash table
+ *   sm_match_prompt     left-to-right, longest-first, non-overlapping spans
+ *                       of a prompt batch
+ *   sm_match_decode     the raw-suffix check after one generated token, with
+ *                       the cache crop it implies
  *
  * General rules for every call
  * ----------------------------
@@ -348,6 +353,96 @@ sm_status sm_prefill_attention(const sm_paged_cache *c, const int32_t *seq_ids,
                                int n, const int32_t *q_offsets, int total_rows,
                                const void *q, int num_q_heads, float scale,
                                int max_rows, void *out, hipStream_t stream);
+
+/*
+ * Merge rules (appendix "Non-overlapping Assignment in a Sequence": R is the
+ * union of the filtered 2-, 3- and 4-gram rules; about 2.17M for the Llama-3
+ * tokenizer).  A rule is four int32: its n >= 2 token ids (>= 0), then -1
+ * for the unused tail.  The table is an open-addressing hash set over
+ * caller-owned device arrays; a built table is read-only.
+ */
+typedef struct {
+  int capacity;      /* slots: a power of two >= 16, and >= 4/3 x the rules */
+  int32_t *keys;     /* [capacity][4]; keys[s][0] == -1 marks an empty slot */
+  int32_t *ids;      /* [capacity] index, in the build's rule list, of the
+                        rule held in slot s (the first one when listed twice) */
+  int32_t *err;      /* [1] sticky error bits */
+} sm_rule_table;
+
+/* Workspace of sm_rules_build: capacity x 8 bytes. */
+size_t sm_rules_build_workspace_bytes(int capacity);
+
+/*
+ * sm_rules_build -- fill the table with rules[0..count) ([count][4], device).
+ *  count  (host) 0 <= count <= 3/4 x capacity (else SM_EINVAL)
+ *  ws     device workspace of sm_rules_build_workspace_bytes(capacity) bytes
+ * Device errors: EINVAL for a malformed rule (fewer than 2 leading ids >= 0,
+ * or a tail entry other than -1): that rule is left out and the table must
+ * be rebuilt.  Slot placement may differ run to run; which keys are present
+ * and their ids do not.
+ */
+sm_status sm_rules_build(const int32_t *rules, int count, const sm_rule_table *t,
+                         void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* sm_rules_lookup -- ids[i] = id of grams[i] ([m][4], same form as a rule)
+ * in R, or -1 (also for a malformed gram). */
+sm_status sm_rules_lookup(const sm_rule_table *t, const int32_t *grams, int m,
+                          int32_t *ids, hipStream_t stream);
+
+/* Workspace of sm_match_prompt: about 17 bytes per token. */
+size_t sm_match_prompt_workspace_bytes(int B, int total_tokens);
+
+/*
+ * sm_match_prompt -- prompt-time span assignment ("Rule Matching"): each
+ * sequence is scanned left to right; at position i the 4-, 3- and then
+ * 2-gram starting there is looked up, the first (longest) rule found becomes
+ * a span and the scan jumps past it, else it steps one token.  A window
+ * never crosses a sequence boundary, and a window holding a negative id
+ * matches nothing.
+ *  token_ids        [total_tokens] int32
+ *  seq_offsets      [B+1] with 0 <= seq_offsets[b] <= seq_offsets[b+1] <=
+ *                   total_tokens; B <= 65535
+ *  span_start       [total_tokens / 2] out: global token index of each span
+ *  span_len         [total_tokens / 2] out: 2..4
+ *  span_rule        [total_tokens / 2] out: rule id
+ *  seq_span_offsets [B+1] out: sequence b's spans are
+ *                   [seq_span_offsets[b], seq_span_offsets[b+1]), in order
+ * The outputs feed sm_pack_spans (span_start, span_len, seq_span_offsets)
+ * and sm_merge_spans (the span's token ids as rows of the embedding table).
+ * Device errors (into t->err): EINVAL for a sequence whose offsets are out
+ * of order or range; it gets no spans.
+ */
+sm_status sm_match_prompt(const sm_rule_table *t, const int32_t *token_ids,
+                          const int32_t *seq_offsets, int B, int total_tokens,
+                          int32_t *span_start, int32_t *span_len,
+                          int32_t *span_rule, int32_t *seq_span_offsets,
+                          void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * sm_match_decode -- the decode-time check after one generated token per
+ * listed sequence ("Decoding-time Integration"): the raw-token suffix ending
+ * at the new token is looked up for n = 4, 3, 2 in turn (only tokens
+ * generated since the sequence's last merge count; a surrogate is never
+ * merged again).  On a match the n tokens become one surrogate: k_out = n-1
+ * cached entries are to be cropped (the new token has no entry yet) and
+ * rule_out = the rule id.  Otherwise k_out = 0, rule_out = -1.
+ *  state      [max_seqs][4] int32 per-sequence match state, device-resident:
+ *             {raw tokens since the last merge (capped at 3), the last three
+ *             of them}; zero it when a sequence starts generating
+ *  seq_ids    [n] distinct ids in [0, max_seqs); n <= 1024
+ *  new_tokens [n] the generated token of each listed sequence
+ *  k_out, rule_out [n] out
+ *  cache      (nullable) if given, sm_kv_rollback(cache, seq_ids, k_out, n)
+ *             runs right after on the same stream: the crop the merges
+ *             imply.  Its device errors go to cache->err; the match state
+ *             is updated either way.
+ * Device errors (into t->err): EINVAL for a bad or repeated id; then no
+ * state changes and every k_out is 0.
+ */
+sm_status sm_match_decode(const sm_rule_table *t, int32_t *state, int max_seqs,
+                          const int32_t *seq_ids, const int32_t *new_tokens,
+                          int n, int32_t *k_out, int32_t *rule_out,
+                          const sm_paged_cache *cache, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -26,7 +26,9 @@ _P, _I, _L, _F, _Z = C.c_void_p, C.c_int, C.c_int64, C.c_float, C.c_size_t
 EXPORTED = ("sm_status_string", "sm_merge_workspace_bytes", "sm_merge_spans",
             "sm_pack_spans", "sm_kv_rollback", "sm_kv_append",
             "sm_decode_workspace_bytes", "sm_decode_attention", "sm_decode_step",
-            "sm_prefill_attention")
+            "sm_prefill_attention", "sm_rules_build_workspace_bytes", "sm_rules_build",
+            "sm_rules_lookup", "sm_match_prompt_workspace_bytes", "sm_match_prompt",
+            "sm_match_decode")
 
 
 class MergeParams(C.Structure):
@@ -41,6 +43,10 @@ class PagedCacheDesc(C.Structure):
                 ("max_blocks_per_seq", _I), ("k_pool", _P), ("v_pool", _P),
                 ("block_table", _P), ("lengths", _P), ("free_stack", _P),
                 ("free_top", _P), ("err", _P)]
+
+
+class RuleTableDesc(C.Structure):
+    _fields_ = [("capacity", _I), ("keys", _P), ("ids", _P), ("err", _P)]
 
 
 class SpanMergeError(RuntimeError):
@@ -83,6 +89,19 @@ def load(path: str = LIB_PATH):
     L.sm_decode_step.restype = _I
     L.sm_prefill_attention.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _I, _P, _I, _F, _I, _P, _P]
     L.sm_prefill_attention.restype = _I
+    L.sm_rules_build_workspace_bytes.argtypes = [_I]
+    L.sm_rules_build_workspace_bytes.restype = _Z
+    L.sm_rules_build.argtypes = [_P, _I, C.POINTER(RuleTableDesc), _P, _Z, _P]
+    L.sm_rules_build.restype = _I
+    L.sm_rules_lookup.argtypes = [C.POINTER(RuleTableDesc), _P, _I, _P, _P]
+    L.sm_rules_lookup.restype = _I
+    L.sm_match_prompt_workspace_bytes.argtypes = [_I, _I]
+    L.sm_match_prompt_workspace_bytes.restype = _Z
+    L.sm_match_prompt.argtypes = [C.POINTER(RuleTableDesc), _P, _P, _I, _I, _P, _P, _P, _P, _P, _Z, _P]
+    L.sm_match_prompt.restype = _I
+    L.sm_match_decode.argtypes = [C.POINTER(RuleTableDesc), _P, _I, _P, _P, _I, _P, _P,
+                                  C.POINTER(PagedCacheDesc), _P]
+    L.sm_match_decode.restype = _I
     _lib = L
     return L
 
@@ -241,3 +260,68 @@ def prefill_attention(cache: PagedCache, seq_ids, q_offsets, q, out, max_rows: i
     st = load().sm_prefill_attention(C.byref(cache.desc), _ptr(seq_ids), seq_ids.numel(), _ptr(q_offsets), rows,
                                      _ptr(q), Hq, sc, max_rows, _ptr(out), _stream(stream))
     _check(st, "sm_prefill_attention")
+
+
+# --------------------------------------------------------------------------
+# merge rules
+
+class RuleTable:
+    """Device buffers of the rule hash table (allocated with torch) and its
+    descriptor.  capacity: a power of two >= 4/3 x the number of rules."""
+
+    def __init__(self, capacity: int, device="cuda"):
+        self.capacity = capacity
+        self.keys = torch.full((capacity, 4), -1, dtype=torch.int32, device=device)
+        self.ids = torch.full((capacity,), -1, dtype=torch.int32, device=device)
+        self.err = torch.zeros(1, dtype=torch.int32, device=device)
+        self.desc = RuleTableDesc(capacity, _ptr(self.keys), _ptr(self.ids), _ptr(self.err))
+
+    @staticmethod
+    def capacity_for(count: int) -> int:
+        c = 16
+        while 3 * c < 4 * count:
+            c *= 2
+        return c
+
+    def error_bits(self) -> int:
+        return int(self.err.item())
+
+    def clear_error(self):
+        self.err.zero_()
+
+
+def rules_build(table: RuleTable, rules, ws=None, stream=None):
+    """rules: [count, 4] int32 on the GPU (n >= 2 ids, then -1)."""
+    need = load().sm_rules_build_workspace_bytes(table.capacity)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=rules.device)
+    st = load().sm_rules_build(_ptr(rules), rules.shape[0], C.byref(table.desc), _ptr(ws),
+                               ws.numel() * ws.element_size(), _stream(stream))
+    _check(st, "sm_rules_build")
+
+
+def rules_lookup(table: RuleTable, grams, ids, stream=None):
+    st = load().sm_rules_lookup(C.byref(table.desc), _ptr(grams), grams.shape[0], _ptr(ids), _stream(stream))
+    _check(st, "sm_rules_lookup")
+
+
+def match_prompt_workspace_bytes(B: int, total_tokens: int) -> int:
+    return load().sm_match_prompt_workspace_bytes(B, total_tokens)
+
+
+def match_prompt(table: RuleTable, token_ids, seq_offsets, span_start, span_len, span_rule,
+                 seq_span_offsets, ws, stream=None):
+    B = seq_offsets.numel() - 1
+    st = load().sm_match_prompt(C.byref(table.desc), _ptr(token_ids), _ptr(seq_offsets), B, token_ids.numel(),
+                                _ptr(span_start), _ptr(span_len), _ptr(span_rule), _ptr(seq_span_offsets),
+                                _ptr(ws), ws.numel() * ws.element_size(), _stream(stream))
+    _check(st, "sm_match_prompt")
+
+
+def match_decode(table: RuleTable, state, seq_ids, new_tokens, k_out, rule_out,
+                 cache: Optional[PagedCache] = None, stream=None):
+    """state [max_seqs, 4] int32 (zeroed when a sequence starts generating)."""
+    st = load().sm_match_decode(C.byref(table.desc), _ptr(state), state.shape[0], _ptr(seq_ids),
+                                _ptr(new_tokens), seq_ids.numel(), _ptr(k_out), _ptr(rule_out),
+                                None if cache is None else C.byref(cache.desc), _stream(stream))
+    _check(st, "sm_match_decode")

@@ -182,6 +182,53 @@ def make_prompts(w: Workload, seed: Optional[int] = None, batch: Optional[int] =
 
 
 # --------------------------------------------------------------------------
+# merge rules: a synthetic stand-in for the rule set mined from WikiText-103
+
+# 2-, 3- and 4-gram rules kept for the Llama-3 tokenizer (the paper's
+# rule-count table, threshold tau = 5)
+RULE_COUNTS_LLAMA3 = (216_700, 684_793, 1_266_080)
+
+
+def make_rules(counts=RULE_COUNTS_LLAMA3, vocab: int = 128256, seed: int = 7) -> np.ndarray:
+    """Distinct uniform random n-grams, counts[n - 2] of each n in 2..4, as
+    [sum(counts), 4] int32 (unused tail -1), in shuffled order."""
+    rng = np.random.RandomState(seed)
+    out = []
+    for n, c in zip((2, 3, 4), counts):
+        got = np.zeros((0, n), np.int64)
+        while len(got) < c:
+            draw = rng.randint(0, vocab, size=(int((c - len(got)) * 1.05) + 16, n))
+            got = np.unique(np.concatenate([got, draw]), axis=0)
+        got = got[rng.permutation(len(got))[:c]]
+        pad = np.full((c, 4), -1, np.int64)
+        pad[:, :n] = got
+        out.append(pad)
+    rules = np.concatenate(out) if out else np.zeros((0, 4), np.int64)
+    return rules[rng.permutation(len(rules))].astype(np.int32)
+
+
+def make_rule_prompts(rules: np.ndarray, B: int, T: int, removal: float, vocab: int, seed: int):
+    """B prompts of T tokens: uniform random ids with randomly chosen rules
+    planted at random non-overlapping places until sum(n - 1) reaches
+    removal x T (the last rule may overshoot by up to 2).  Returns
+    (token_ids [B T] int32, seq_offsets [B + 1] int32)."""
+    rng = np.random.RandomState(seed)
+    n_of = (rules >= 0).sum(1)
+    toks = rng.randint(0, vocab, size=B * T).astype(np.int32)
+    target = int(round(removal * T))
+    for b in range(B):
+        picked, cost = [], 0
+        while cost < target and len(rules):
+            r = int(rng.randint(len(rules)))
+            picked.append(r)
+            cost += int(n_of[r]) - 1
+        starts, _ = layout_spans(rng, T, n_of[picked])
+        for st, r in zip(starts, picked):
+            toks[b * T + st:b * T + st + n_of[r]] = rules[r, :n_of[r]]
+    return toks, (np.arange(B + 1) * T).astype(np.int32)
+
+
+# --------------------------------------------------------------------------
 # floating tensors
 
 def generator(seed: int, device="cpu") -> torch.Generator:

@@ -126,3 +126,31 @@ def test_pack_argument_checks(L):
     assert L.sm_pack_spans(0, 1, 0, 0, 1, 1, 1, 1, 1, 1, None, None, 0, None, 0, 1, None, 1, None) == sm.SM_OK
     # rows requested without an embedding table
     assert L.sm_pack_spans(2, 1, 8, 1, 1, 1, 1, 1, 1, 1, None, None, 0, None, 64, 1, 1, 1, None) == sm.SM_EINVAL
+
+
+def test_rule_call_argument_checks(L):
+    good = sm.RuleTableDesc(1024, 1, 1, 1)
+    bad_cap = sm.RuleTableDesc(1000, 1, 1, 1)               # not a power of two
+    assert L.sm_rules_build_workspace_bytes(1024) == 8192
+    assert L.sm_rules_build(1, 10, C.byref(bad_cap), 1, 1 << 20, None) == sm.SM_EINVAL
+    assert L.sm_rules_build(1, 769, C.byref(good), 1, 1 << 20, None) == sm.SM_EINVAL   # load above 3/4
+    assert L.sm_rules_build(1, 10, C.byref(good), 1, 8191, None) == sm.SM_EINVAL       # workspace
+    assert L.sm_rules_build(1, 10, C.byref(good), None, 1 << 20, None) == sm.SM_EINVAL
+    assert L.sm_rules_build(None, 10, C.byref(good), 1, 1 << 20, None) == sm.SM_EINVAL
+    assert L.sm_rules_lookup(C.byref(good), 1, 0, 1, None) == sm.SM_OK                 # nothing to do
+    assert L.sm_rules_lookup(C.byref(bad_cap), 1, 4, 1, None) == sm.SM_EINVAL
+    assert L.sm_rules_lookup(C.byref(good), None, 4, 1, None) == sm.SM_EINVAL
+    need = L.sm_match_prompt_workspace_bytes(16, 65536)
+    assert need >= 17 * 65536
+    mp = lambda ws_bytes, B=16, T=65536, tbl=good, sso=1: L.sm_match_prompt(
+        C.byref(tbl), 1, 1, B, T, 1, 1, 1, sso, 1, ws_bytes, None)
+    assert mp(need - 1) == sm.SM_EINVAL
+    assert mp(need, B=70000) == sm.SM_EINVAL
+    assert mp(need, tbl=bad_cap) == sm.SM_EINVAL
+    assert mp(need, sso=None) == sm.SM_EINVAL
+    md = lambda n, ids=1, cache=None: L.sm_match_decode(C.byref(good), 1, 64, ids, 1, n, 1, 1, cache, None)
+    assert md(0) == sm.SM_OK
+    assert md(1025) == sm.SM_EINVAL
+    assert md(4, ids=None) == sm.SM_EINVAL
+    assert md(4, cache=C.byref(_desc(head_dim=96))) == sm.SM_EINVAL                      # the rollback's checks
+    assert md(5, cache=C.byref(_desc())) == sm.SM_EINVAL                                 # n > max_seqs (4)
