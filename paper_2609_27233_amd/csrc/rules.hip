@@ -74,6 +74,47 @@ __device__ __forceinline__ int rule_find(const i32x4_t *keys, const int32_t *ids
   return -1;
 }
 
+// The longest of up to three candidate keys (cand[0] the longest) that is a
+// rule: the three probe chains advance together, so their memory latencies
+// overlap instead of adding up.  want[c] = false skips a candidate.  Returns
+// the index of the winning candidate (or -1) and its rule id in *id.
+__device__ __forceinline__ int rule_find_longest(const i32x4_t *keys, const int32_t *ids, uint32_t mask,
+                                                 const i32x4_t (&cand)[3], const bool (&want)[3], int *id) {
+  uint32_t slot[3];
+  int state[3];  // -2 probing, -1 absent, else the slot that holds it
+#pragma unroll
+  for (int c = 0; c < 3; ++c) {
+    slot[c] = (uint32_t)rule_hash(cand[c]) & mask;
+    state[c] = want[c] ? -2 : -1;
+  }
+  for (uint32_t p = 0; p <= mask; ++p) {
+    i32x4_t e[3];
+#pragma unroll
+    for (int c = 0; c < 3; ++c)
+      if (state[c] == -2) e[c] = keys[slot[c]];
+    bool busy = false;
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+      if (state[c] != -2) continue;
+      if (e[c].x == -1) state[c] = -1;
+      else if (key_eq(e[c], cand[c])) state[c] = (int)slot[c];
+      else {
+        slot[c] = (slot[c] + 1) & mask;
+        busy = true;
+      }
+    }
+    if (!busy) break;
+  }
+#pragma unroll
+  for (int c = 0; c < 3; ++c)
+    if (state[c] >= 0) {
+      *id = ids[state[c]];
+      return c;
+    }
+  *id = -1;
+  return -1;
+}
+
 // ---- build ----------------------------------------------------------------
 
 __global__ void rules_clear_kernel(uint64_t *claim, int cap) {
@@ -145,21 +186,20 @@ __global__ void match_len_kernel(const i32x4_t *keys, const int32_t *ids, uint32
   int x[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) x[j] = t + j < end ? tokens[t + j] : -1;
-  int len = 0, id = -1;
+  i32x4_t cand[3];
+  bool want[3];
 #pragma unroll
-  for (int n = 4; n >= 2; --n) {
-    if (len || t + n > end) continue;
-    bool neg = false;
+  for (int c = 0; c < 3; ++c) {  // candidate c: the (4 - c)-gram at t
+    const int n = 4 - c;
+    bool ok = t + n <= end;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) neg |= j < n && x[j] < 0;
-    if (neg) continue;
-    const i32x4_t k{x[0], x[1], n > 2 ? x[2] : -1, n > 3 ? x[3] : -1};
-    const int f = rule_find(keys, ids, mask, k);
-    if (f >= 0) {
-      len = n;
-      id = f;
-    }
+    for (int j = 0; j < 4; ++j) ok = ok && (j >= n || x[j] >= 0);
+    want[c] = ok;
+    cand[c] = i32x4_t{x[0], x[1], n > 2 ? x[2] : -1, n > 3 ? x[3] : -1};
   }
+  int id;
+  const int c = rule_find_longest(keys, ids, mask, cand, want, &id);
+  const int len = c >= 0 ? 4 - c : 0;
   mlen[t] = (int8_t)len;
   rid[t] = id;
 }
@@ -311,21 +351,20 @@ __global__ __launch_bounds__(kDecThreads) void match_decode_kernel(const i32x4_t
   const i32x4_t st = state[s];
   const int r = min(max(st.x, 0), 3);  // raw tokens since the last merge, at most 3 kept
   const int w[4] = {st.y, st.z, st.w, new_tokens[i]};
-  int k = 0, id = -1;
+  i32x4_t cand[3];
+  bool want[3];
 #pragma unroll
-  for (int m = 4; m >= 2; --m) {
-    if (id >= 0 || m > r + 1) continue;
-    bool neg = false;
+  for (int c = 0; c < 3; ++c) {  // candidate c: the suffix of m = 4 - c tokens
+    const int m = 4 - c;
+    bool ok = m <= r + 1;
 #pragma unroll
-    for (int j = 4 - m; j < 4; ++j) neg |= w[j] < 0;
-    if (neg) continue;
-    const i32x4_t key{w[4 - m], w[5 - m], m > 2 ? w[6 - m] : -1, m > 3 ? w[3] : -1};
-    const int f = rule_find(keys, ids, mask, key);
-    if (f >= 0) {
-      id = f;
-      k = m - 1;
-    }
+    for (int j = 0; j < 4; ++j) ok = ok && (j < 4 - m || w[j] >= 0);
+    want[c] = ok;
+    cand[c] = i32x4_t{w[4 - m], w[5 - m], m > 2 ? w[6 - m] : -1, m > 3 ? w[3] : -1};
   }
+  int id;
+  const int c = rule_find_longest(keys, ids, mask, cand, want, &id);
+  const int k = c >= 0 ? 3 - c : 0;  // n - 1 entries to crop
   state[s] = id >= 0 ? i32x4_t{0, -1, -1, -1} : i32x4_t{min(r + 1, 3), w[1], w[2], w[3]};
   k_out[i] = k;
   rule_out[i] = id;

@@ -197,8 +197,10 @@ def make_rules(counts=RULE_COUNTS_LLAMA3, vocab: int = 128256, seed: int = 7) ->
     for n, c in zip((2, 3, 4), counts):
         got = np.zeros((0, n), np.int64)
         while len(got) < c:
-            draw = rng.randint(0, vocab, size=(int((c - len(got)) * 1.05) + 16, n))
-            got = np.unique(np.concatenate([got, draw]), axis=0)
+            draw = np.concatenate([got, rng.randint(0, vocab, size=(int((c - len(got)) * 1.05) + 16, n))])
+            rows = np.ascontiguousarray(draw).view(np.dtype((np.void, 8 * n))).ravel()
+            _, first = np.unique(rows, return_index=True)          # distinct rows
+            got = draw[np.sort(first)]
         got = got[rng.permutation(len(got))[:c]]
         pad = np.full((c, 4), -1, np.int64)
         pad[:, :n] = got
