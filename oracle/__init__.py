@@ -98,6 +98,10 @@ def _declare(L):
     L.orc_match_decode_step.argtypes = [C.POINTER(_Rules), _P, C.POINTER(_I), C.c_int32, C.POINTER(C.c_int32),
                                         C.POINTER(C.c_int32)]
     L.orc_match_decode_step.restype = None
+    L.orc_gather_surrogates.argtypes = [_P, _L, _P, _L, _P, _P, _I, _I, _I, _P]
+    L.orc_gather_surrogates.restype = _I
+    L.orc_span_dedupe.argtypes = [_P, _P, _P, _I, _I, _P, _P, _P, _P, _P]
+    L.orc_span_dedupe.restype = _I
     L.orc_num_threads.argtypes = []
     L.orc_num_threads.restype = _I
 
@@ -356,3 +360,33 @@ class OracleRules:
     def state(self, seq):
         buf, n = self._states.get(seq, (np.zeros(0, np.int32), 0))
         return buf[:n].copy()
+
+
+# --------------------------------------------------------------------------
+# surrogate lookup and span dedupe
+
+def gather_surrogates(emb, lut, token_ids, rule_ids):
+    """out[i] = lut[rule_ids[i]] if rule_ids[i] >= 0 else emb[token_ids[i]];
+    emb, lut: raw element arrays [rows, d] of one dtype.  (status, out)."""
+    emb, lut = np.ascontiguousarray(emb), np.ascontiguousarray(lut)
+    rule_ids = _i32(rule_ids)
+    tok = None if token_ids is None else _i32(token_ids)
+    n, d = rule_ids.shape[0], lut.shape[1]
+    out = np.zeros((n, d), dtype=lut.dtype)
+    st = lib().orc_gather_surrogates(_ptr(emb), emb.shape[0], _ptr(lut), lut.shape[0], _ptr(tok),
+                                     _ptr(rule_ids), n, d, lut.dtype.itemsize, _ptr(out))
+    return st, out
+
+
+def span_dedupe(span_rule, span_start, span_len, num_rules, token_ids):
+    """(U, uniq_span [U], span_slot [S], uniq_row_idx, uniq_span_offsets [U+1])."""
+    r, st_, ln, tok = _i32(span_rule), _i32(span_start), _i32(span_len), _i32(token_ids)
+    S = r.shape[0]
+    us, slot = np.zeros(max(S, 1), np.int32), np.zeros(max(S, 1), np.int32)
+    rows = np.zeros(max(int(ln.sum()), 1), np.int32)
+    offs = np.zeros(S + 1, np.int32)
+    U = lib().orc_span_dedupe(_ptr(r), _ptr(st_), _ptr(ln), S, num_rules, _ptr(tok), _ptr(us), _ptr(slot),
+                              _ptr(rows), _ptr(offs))
+    if U < 0:
+        return U, None, None, None, None
+    return U, us[:U].copy(), slot[:S].copy(), rows[:offs[U]].copy(), offs[:U + 1].copy()

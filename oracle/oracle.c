@@ -673,3 +673,56 @@ void orc_match_decode_step(const orc_rules *r, int32_t *state, int *state_len,
     return;
   }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Surrogate lookup and span dedupe ("Computational Scope").                */
+
+int orc_gather_surrogates(const void *emb, int64_t emb_rows, const void *lut,
+                          int64_t lut_rows, const int32_t *token_ids,
+                          const int32_t *rule_ids, int n, int d,
+                          int elem_bytes, void *out) {
+  int st = ORC_OK;
+  for (int i = 0; i < n; ++i) {
+    const char *src = NULL;
+    if (rule_ids[i] >= 0) {
+      if (rule_ids[i] < lut_rows) src = (const char *)lut + (int64_t)rule_ids[i] * d * elem_bytes;
+    } else if (token_ids && token_ids[i] >= 0 && token_ids[i] < emb_rows) {
+      src = (const char *)emb + (int64_t)token_ids[i] * d * elem_bytes;
+    }
+    char *dst = (char *)out + (int64_t)i * d * elem_bytes;
+    if (src) {
+      for (int64_t b = 0; b < (int64_t)d * elem_bytes; ++b) dst[b] = src[b];
+    } else {
+      for (int64_t b = 0; b < (int64_t)d * elem_bytes; ++b) dst[b] = 0;
+      st = ORC_EINVAL;
+    }
+  }
+  return st;
+}
+
+int orc_span_dedupe(const int32_t *span_rule, const int32_t *span_start,
+                    const int32_t *span_len, int S, int num_rules,
+                    const int32_t *token_ids, int32_t *uniq_span,
+                    int32_t *span_slot, int32_t *uniq_row_idx,
+                    int32_t *uniq_span_offsets) {
+  for (int s = 0; s < S; ++s)
+    if (span_rule[s] < 0 || span_rule[s] >= num_rules) return -1;
+  int U = 0;
+  uniq_span_offsets[0] = 0;
+  for (int s = 0; s < S; ++s) {
+    int first = -1; /* an earlier span with the same rule */
+    for (int p = 0; p < s && first < 0; ++p)
+      if (span_rule[p] == span_rule[s]) first = p;
+    if (first < 0) {
+      span_slot[s] = U;
+      uniq_span[U] = s;
+      const int off = uniq_span_offsets[U];
+      for (int j = 0; j < span_len[s]; ++j) uniq_row_idx[off + j] = token_ids[span_start[s] + j];
+      uniq_span_offsets[U + 1] = off + span_len[s];
+      ++U;
+    } else {
+      span_slot[s] = span_slot[first];
+    }
+  }
+  return U;
+}

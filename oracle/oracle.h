@@ -130,6 +130,29 @@ int orc_match_prompt(const orc_rules *r, int B, const int32_t *seq_offsets,
 void orc_match_decode_step(const orc_rules *r, int32_t *state, int *state_len,
                            int32_t token, int32_t *k_out, int32_t *rule_out);
 
+/* Surrogate lookup ("Computational Scope": a span's surrogate depends on
+ * its tokens only, so surrogates can be precomputed per rule and looked
+ * up).  out[i] = lut[rule_ids[i]] when rule_ids[i] >= 0, else
+ * emb[token_ids[i]]: the step input of a decode step (surrogate or plain
+ * token) and the surrogates of a prompt's spans.  Rows are raw elements of
+ * elem_bytes; an index out of range gives EINVAL and a zero row. */
+int orc_gather_surrogates(const void *emb, int64_t emb_rows, const void *lut,
+                          int64_t lut_rows, const int32_t *token_ids,
+                          const int32_t *rule_ids, int n, int d,
+                          int elem_bytes, void *out);
+
+/* Span dedupe within one merge batch: spans with the same rule share one
+ * surrogate.  uniq_span[u] = the u-th span (in order) whose rule has not
+ * occurred before it; span_slot[s] = u of the first span with s's rule;
+ * returns the number of unique spans (or -1 for a rule id outside
+ * [0, num_rules)).  The unique spans' rows for the merge module come out
+ * as CSR: uniq_row_idx (token ids) and uniq_span_offsets [U + 1]. */
+int orc_span_dedupe(const int32_t *span_rule, const int32_t *span_start,
+                    const int32_t *span_len, int S, int num_rules,
+                    const int32_t *token_ids, int32_t *uniq_span,
+                    int32_t *span_slot, int32_t *uniq_row_idx,
+                    int32_t *uniq_span_offsets);
+
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int orc_num_threads(void);
 
