@@ -26,6 +26,8 @@
  *                       of a prompt batch
  *   sm_match_decode     the raw-suffix check after one generated token, with
  *                       the cache crop it implies
+ *   sm_gather_surrogates surrogates looked up per rule (or plain token rows)
+ *   sm_span_dedupe      one surrogate per distinct rule in a merge batch
  *
  * General rules for every call
  * ----------------------------
@@ -443,6 +445,59 @@ sm_status sm_match_decode(const sm_rule_table *t, int32_t *state, int max_seqs,
                           const int32_t *seq_ids, const int32_t *new_tokens,
                           int n, int32_t *k_out, int32_t *rule_out,
                           const sm_paged_cache *cache, hipStream_t stream);
+
+/*
+ * Surrogate lookup ("Computational Scope": a span's surrogate depends on its
+ * tokens only, so frequently used surrogates can be precomputed and looked
+ * up).  A lookup table is any [lut_rows][d] array of surrogates indexed by
+ * rule id, for instance sm_merge_spans run once over the rule list.
+ *
+ * sm_gather_surrogates -- out[i] = lut[rule_ids[i]] if rule_ids[i] >= 0,
+ * else emb[token_ids[i]] (a decode step's input: the surrogate of a
+ * just-merged suffix or the plain token; or a prompt's span surrogates for
+ * sm_pack_spans).  Bit-exact row copies.
+ *  emb        [emb_rows][d] embedding table (may be null with token_ids null)
+ *  lut        [lut_rows][d] surrogates by rule id
+ *  token_ids  [n] nullable: without it every rule id must be >= 0
+ *  rule_ids   [n]
+ *  d          (host) (d x element bytes) a multiple of 16
+ *  out        [n][d] (dtype dt)
+ * Device errors: EINVAL for an index out of range; that row is zero.
+ */
+sm_status sm_gather_surrogates(const void *emb, int64_t emb_rows,
+                               const void *lut, int64_t lut_rows,
+                               const int32_t *token_ids, const int32_t *rule_ids,
+                               int n, int d, sm_dtype dt, void *out,
+                               int32_t *err, hipStream_t stream);
+
+/* Workspace of sm_span_dedupe: 4 bytes per rule and per span, plus 512. */
+size_t sm_span_dedupe_workspace_bytes(int S, int num_rules);
+
+/*
+ * sm_span_dedupe -- spans of one merge batch that carry the same rule share
+ * one surrogate.  For spans s = 0..S-1 (e.g. from sm_match_prompt):
+ *  uniq_span[u]   the u-th span, in order, whose rule did not occur before
+ *                 it (u < *num_uniq)
+ *  span_slot[s]   u of the first span with s's rule
+ *  uniq_row_idx, uniq_span_offsets [*num_uniq + 1]: the unique spans' token
+ *                 ids as CSR rows, the input of sm_merge_spans; then
+ *                 sm_gather_surrogates(lut = its output, rule_ids = span_slot)
+ *                 gives every span's surrogate.
+ *  num_uniq       [1] out (device); the caller reads it to size the merge
+ *  span_rule      [S] rule ids in [0, num_rules)
+ *  span_start, span_len [S] global token index and length (>= 1) of each span
+ *  token_ids      [total_tokens]
+ *  uniq_row_idx   capacity: sum of span_len
+ * Device errors: EINVAL for a rule id or span range out of bounds; then
+ * *num_uniq = 0 and the other outputs are unspecified.
+ */
+sm_status sm_span_dedupe(const int32_t *span_rule, const int32_t *span_start,
+                         const int32_t *span_len, int S, int num_rules,
+                         const int32_t *token_ids, int total_tokens,
+                         int32_t *uniq_span, int32_t *span_slot,
+                         int32_t *uniq_row_idx, int32_t *uniq_span_offsets,
+                         int32_t *num_uniq, void *ws, size_t ws_bytes,
+                         int32_t *err, hipStream_t stream);
 
 #ifdef __cplusplus
 }

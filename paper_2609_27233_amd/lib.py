@@ -28,7 +28,7 @@ EXPORTED = ("sm_status_string", "sm_merge_workspace_bytes", "sm_merge_spans",
             "sm_decode_workspace_bytes", "sm_decode_attention", "sm_decode_step",
             "sm_prefill_attention", "sm_rules_build_workspace_bytes", "sm_rules_build",
             "sm_rules_lookup", "sm_match_prompt_workspace_bytes", "sm_match_prompt",
-            "sm_match_decode")
+            "sm_match_decode", "sm_gather_surrogates", "sm_span_dedupe_workspace_bytes", "sm_span_dedupe")
 
 
 class MergeParams(C.Structure):
@@ -102,6 +102,12 @@ def load(path: str = LIB_PATH):
     L.sm_match_decode.argtypes = [C.POINTER(RuleTableDesc), _P, _I, _P, _P, _I, _P, _P,
                                   C.POINTER(PagedCacheDesc), _P]
     L.sm_match_decode.restype = _I
+    L.sm_gather_surrogates.argtypes = [_P, _L, _P, _L, _P, _P, _I, _I, _I, _P, _P, _P]
+    L.sm_gather_surrogates.restype = _I
+    L.sm_span_dedupe_workspace_bytes.argtypes = [_I, _I]
+    L.sm_span_dedupe_workspace_bytes.restype = _Z
+    L.sm_span_dedupe.argtypes = [_P, _P, _P, _I, _I, _P, _I, _P, _P, _P, _P, _P, _P, _Z, _P, _P]
+    L.sm_span_dedupe.restype = _I
     _lib = L
     return L
 
@@ -325,3 +331,28 @@ def match_decode(table: RuleTable, state, seq_ids, new_tokens, k_out, rule_out,
                                 _ptr(new_tokens), seq_ids.numel(), _ptr(k_out), _ptr(rule_out),
                                 None if cache is None else C.byref(cache.desc), _stream(stream))
     _check(st, "sm_match_decode")
+
+
+# --------------------------------------------------------------------------
+# surrogate lookup and span dedupe
+
+def gather_surrogates(lut, rule_ids, out, err, emb=None, token_ids=None, stream=None):
+    """out[i] = lut[rule_ids[i]] if rule_ids[i] >= 0 else emb[token_ids[i]]."""
+    n, d = out.shape
+    st = load().sm_gather_surrogates(_ptr(emb), 0 if emb is None else emb.shape[0], _ptr(lut), lut.shape[0],
+                                     _ptr(token_ids), _ptr(rule_ids), n, d, dtype_code(out.dtype), _ptr(out),
+                                     _ptr(err), _stream(stream))
+    _check(st, "sm_gather_surrogates")
+
+
+def span_dedupe(span_rule, span_start, span_len, num_rules, token_ids, uniq_span, span_slot, uniq_row_idx,
+                uniq_span_offsets, num_uniq, err, ws=None, stream=None):
+    S = span_rule.numel()
+    need = load().sm_span_dedupe_workspace_bytes(S, num_rules)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=span_rule.device)
+    st = load().sm_span_dedupe(_ptr(span_rule), _ptr(span_start), _ptr(span_len), S, num_rules, _ptr(token_ids),
+                               token_ids.numel(), _ptr(uniq_span), _ptr(span_slot), _ptr(uniq_row_idx),
+                               _ptr(uniq_span_offsets), _ptr(num_uniq), _ptr(ws), ws.numel() * ws.element_size(),
+                               _ptr(err), _stream(stream))
+    _check(st, "sm_span_dedupe")

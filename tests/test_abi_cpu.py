@@ -154,3 +154,20 @@ def test_rule_call_argument_checks(L):
     assert md(4, ids=None) == sm.SM_EINVAL
     assert md(4, cache=C.byref(_desc(head_dim=96))) == sm.SM_EINVAL                      # the rollback's checks
     assert md(5, cache=C.byref(_desc())) == sm.SM_EINVAL                                 # n > max_seqs (4)
+
+
+def test_lut_call_argument_checks(L):
+    g = lambda n=4, d=64, dt=sm.SM_BF16, rule=1, out=1, err=1: L.sm_gather_surrogates(
+        1, 10, 1, 10, 1, rule, n, d, dt, out, err, None)
+    assert g(n=0) == sm.SM_OK
+    assert g(n=-1) == sm.SM_EINVAL
+    assert g(d=4) == sm.SM_EINVAL                       # 8 bytes: not a multiple of 16
+    assert g(dt=7) == sm.SM_EINVAL
+    assert g(rule=None) == sm.SM_EINVAL and g(out=None) == sm.SM_EINVAL and g(err=None) == sm.SM_EINVAL
+    need = L.sm_span_dedupe_workspace_bytes(100, 1000)
+    assert need >= 4 * 1100
+    dd = lambda ws_bytes=need, S=100, rule=1: L.sm_span_dedupe(rule, 1, 1, S, 1000, 1, 500, 1, 1, 1, 1, 1, 1,
+                                                               ws_bytes, 1, None)
+    assert dd(ws_bytes=need - 1) == sm.SM_EINVAL
+    assert dd(S=-1) == sm.SM_EINVAL
+    assert dd(rule=None) == sm.SM_EINVAL
