@@ -394,6 +394,7 @@ def extras_report(job, stream, attn_us):
     out["merge_spans_70b_prompt_batch"] = merge_70b_report(job.sm, job.L, dev, stream)
     out["prefill_attention"] = prefill_report(job.sm, job.L, dev, stream)
     out["rule_matching"] = rules_report(job.sm, job.L, dev, stream)
+    out["surrogate_lookup"] = lut_report(job.sm, job.L, dev, stream)
     return out
 
 
@@ -536,6 +537,100 @@ def rules_report(sm, L, dev, stream, reps=20):
                 f"{t.capacity * 20 / 2**20:.0f} MiB table"}
 
 
+def lut_report(sm, L, dev, stream, reps=20):
+    """Surrogates of the 16 x 4096 prompt batch's matched spans (d = 4096,
+    bf16): looked up by rule id in a table of all 2.17M rules (17.8 GB),
+    against the merge module over the same spans; the decode-step input of
+    16 sequences; and the dedupe of a batch whose rules follow a Zipf law."""
+    import torch
+    from paper_2609_27233_amd import workload as wl
+    st = stream.cuda_stream
+    w = wl.WORKLOADS[2]
+    d, h = w.d, w.h
+    rules_np = wl.make_rules()
+    R = len(rules_np)
+    i32 = lambda a: torch.as_tensor(np.asarray(a, np.int32)).to(dev)
+    toks_np, offs_np = wl.make_rule_prompts(rules_np, 16, 4096, 0.4, w.vocab, seed=3)
+    t = sm.RuleTable(sm.RuleTable.capacity_for(R), device=dev)
+    sm.rules_build(t, i32(rules_np))
+    T, B = len(toks_np), 16
+    toks, offs = i32(toks_np), i32(offs_np)
+    s0, ln, ru = (torch.empty(T // 2, dtype=torch.int32, device=dev) for _ in range(3))
+    sso = torch.empty(B + 1, dtype=torch.int32, device=dev)
+    sm.match_prompt(t, toks, offs, s0, ln, ru, sso,
+                    torch.empty(sm.match_prompt_workspace_bytes(B, T), dtype=torch.uint8, device=dev))
+    S = int(sso[-1].item())
+    g = wl.generator(5, dev)
+    emb = wl.randn((w.vocab, d), torch.bfloat16, g, device=dev, std=0.02)
+    lut = torch.empty((R, d), dtype=torch.bfloat16, device=dev)      # values do not change a copy's cost
+    z = torch.empty((S, d), dtype=torch.bfloat16, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def gather():
+        if L.sm_gather_surrogates(None, 0, lut.data_ptr(), R, None, ru.data_ptr(), S, d, sm.SM_BF16, z.data_ptr(),
+                                  err.data_ptr(), st):
+            raise RuntimeError("sm_gather_surrogates failed")
+    t_g = _time(gather, stream, reps)
+    # the merge module over the same spans
+    ln_h, s0_h = ln[:S].cpu().numpy(), s0[:S].cpu().numpy()
+    rows = i32(np.concatenate([toks_np[a:a + n] for a, n in zip(s0_h, ln_h)]))
+    so = i32(np.concatenate([[0], np.cumsum(ln_h)]))
+    par = wl.make_merge_params(d, h, torch.bfloat16, g, device=dev)
+    ws = torch.empty(sm.merge_workspace_bytes(rows.numel(), S, d, torch.bfloat16), dtype=torch.uint8, device=dev)
+    mp = sm.MergeParams(d, h, 1e-5, *(par[k].data_ptr() for k in
+                        ("Q", "W_kv", "b_kv", "g_kv", "beta_kv", "W_o", "b_o", "g_o", "beta_o")))
+
+    def merge():
+        if L.sm_merge_spans(emb.data_ptr(), emb.shape[0], rows.data_ptr(), rows.numel(), so.data_ptr(), S,
+                            C.byref(mp), sm.SM_BF16, z.data_ptr(), ws.data_ptr(), ws.numel(), err.data_ptr(), st):
+            raise RuntimeError("sm_merge_spans failed")
+    t_m = _time(merge, stream, 3)
+    del ws
+    # decode step inputs: 16 sequences, half of them just merged
+    rid16 = i32(np.where(np.arange(16) % 2 == 0, np.arange(16) * 1000, -1))
+    tok16 = i32(np.arange(16) * 7)
+    x16 = torch.empty((16, d), dtype=torch.bfloat16, device=dev)
+
+    def step_in():
+        if L.sm_gather_surrogates(emb.data_ptr(), emb.shape[0], lut.data_ptr(), R, tok16.data_ptr(),
+                                  rid16.data_ptr(), 16, d, sm.SM_BF16, x16.data_ptr(), err.data_ptr(), st):
+            raise RuntimeError("sm_gather_surrogates failed")
+    t_s = _time(step_in, stream, 100)
+    del lut
+    torch.cuda.empty_cache()
+    # dedupe of a batch with Zipf-distributed rules
+    tz_np, oz_np = wl.make_rule_prompts(rules_np, 16, 4096, 0.4, w.vocab, seed=9, zipf_a=1.2)
+    tz = i32(tz_np)
+    sm.match_prompt(t, tz, i32(oz_np), s0, ln, ru, sso,
+                    torch.empty(sm.match_prompt_workspace_bytes(B, T), dtype=torch.uint8, device=dev))
+    Sz = int(sso[-1].item())
+    nsum = int(ln[:Sz].sum().item())
+    uq, slot = (torch.empty(Sz, dtype=torch.int32, device=dev) for _ in range(2))
+    urows, uoffs = torch.empty(nsum, dtype=torch.int32, device=dev), torch.empty(Sz + 1, dtype=torch.int32, device=dev)
+    nu = torch.zeros(1, dtype=torch.int32, device=dev)
+    wsd = torch.empty(L.sm_span_dedupe_workspace_bytes(Sz, R), dtype=torch.uint8, device=dev)
+
+    def dedupe():
+        if L.sm_span_dedupe(ru.data_ptr(), s0.data_ptr(), ln.data_ptr(), Sz, R, tz.data_ptr(), T, uq.data_ptr(),
+                            slot.data_ptr(), urows.data_ptr(), uoffs.data_ptr(), nu.data_ptr(), wsd.data_ptr(),
+                            wsd.numel(), err.data_ptr(), st):
+            raise RuntimeError("sm_span_dedupe failed")
+    t_d = _time(dedupe, stream, reps)
+    U = int(nu.item())
+    assert int(err.item()) == 0 and t.error_bits() == 0
+    gbytes = 2.0 * S * d * 2
+    return {
+        "spans": S, "table_rows": R, "table_GB": round(R * d * 2 / 1e9, 1),
+        "gather_us": round(t_g * 1e3, 1), "gather_GBps": round(gbytes / (t_g * 1e-3) / 1e9, 1),
+        "gather_frac_of_hbm_peak": round(gbytes / (t_g * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "merge_module_same_spans_ms": round(t_m, 3), "lookup_speedup": round(t_m / t_g, 1),
+        "decode_step_inputs_16_us": round(t_s * 1e3, 2),
+        "zipf_batch_spans": Sz, "zipf_batch_distinct": U, "dedupe_us": round(t_d * 1e3, 1),
+        "note": "HIP events around back-to-back calls; gather bytes = read + write of the span rows; the table "
+                "is allocated at full size (values do not change a copy); dedupe on a batch whose planted rules "
+                "follow Zipf(1.2) over the rule list"}
+
+
 def traffic_bytes(alg_bytes):
     """Measured HBM bytes per attention launch, or None when the kernel
     sources differ from the ones the counters were taken on."""
@@ -628,6 +723,8 @@ def main():
                     help="only run a plain device copy of BYTES three times (scales HBM counters) and exit")
     ap.add_argument("--merge-only", action="store_true",
                     help="only time the merge module over the 70B-shaped prompt batch and print that")
+    ap.add_argument("--lut-only", action="store_true",
+                    help="only time the surrogate lookup, the merge module on the same spans, and the dedupe")
     ap.add_argument("--rules-only", action="store_true",
                     help="only time the rule table build and the prompt / decode matching")
     ap.add_argument("--prefill-only", action="store_true",
@@ -657,6 +754,10 @@ def main():
     if args.merge_only:
         from paper_2609_27233_amd import lib as sm
         print(json.dumps(merge_70b_report(sm, sm.load(), dev, torch.cuda.current_stream(), reps=5)), flush=True)
+        return
+    if args.lut_only:
+        from paper_2609_27233_amd import lib as sm
+        print(json.dumps(lut_report(sm, sm.load(), dev, torch.cuda.current_stream())), flush=True)
         return
     if args.rules_only:
         from paper_2609_27233_amd import lib as sm

@@ -57,7 +57,7 @@ __global__ void dedupe_owner_kernel(const int32_t *span_rule, const int32_t *spa
     atomicOr(flag, 1);
     return;
   }
-  atomicMin(&owner[r], s);
+  if (__atomic_load_n(&owner[r], __ATOMIC_RELAXED) > s) atomicMin(&owner[r], s);  // skip when already beaten
 }
 
 // one workgroup: unique spans in order and their CSR row offsets

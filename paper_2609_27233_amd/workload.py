@@ -209,10 +209,13 @@ def make_rules(counts=RULE_COUNTS_LLAMA3, vocab: int = 128256, seed: int = 7) ->
     return rules[rng.permutation(len(rules))].astype(np.int32)
 
 
-def make_rule_prompts(rules: np.ndarray, B: int, T: int, removal: float, vocab: int, seed: int):
+def make_rule_prompts(rules: np.ndarray, B: int, T: int, removal: float, vocab: int, seed: int,
+                      zipf_a: Optional[float] = None):
     """B prompts of T tokens: uniform random ids with randomly chosen rules
     planted at random non-overlapping places until sum(n - 1) reaches
-    removal x T (the last rule may overshoot by up to 2).  Returns
+    removal x T (the last rule may overshoot by up to 2).  Rules are drawn
+    uniformly, or with zipf_a by a Zipf law over the rule list's order (a
+    stand-in for n-gram frequencies of real text).  Returns
     (token_ids [B T] int32, seq_offsets [B + 1] int32)."""
     rng = np.random.RandomState(seed)
     n_of = (rules >= 0).sum(1)
@@ -221,7 +224,7 @@ def make_rule_prompts(rules: np.ndarray, B: int, T: int, removal: float, vocab: 
     for b in range(B):
         picked, cost = [], 0
         while cost < target and len(rules):
-            r = int(rng.randint(len(rules)))
+            r = int(rng.randint(len(rules))) if zipf_a is None else int(rng.zipf(zipf_a) - 1) % len(rules)
             picked.append(r)
             cost += int(n_of[r]) - 1
         starts, _ = layout_spans(rng, T, n_of[picked])
