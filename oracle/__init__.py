@@ -102,6 +102,8 @@ def _declare(L):
     L.orc_gather_surrogates.restype = _I
     L.orc_span_dedupe.argtypes = [_P, _P, _P, _I, _I, _P, _P, _P, _P, _P]
     L.orc_span_dedupe.restype = _I
+    L.orc_kv_project.argtypes = [C.POINTER(_Cache), _P, _I, _P, _I, _P, _P, _D, _D, _P, _P]
+    L.orc_kv_project.restype = _I
     L.orc_num_threads.argtypes = []
     L.orc_num_threads.restype = _I
 
@@ -263,6 +265,17 @@ class OracleCache:
         st = lib().orc_prefill_attention(C.byref(s), _ptr(seq_ids), seq_ids.shape[0],
                                          _ptr(q_offsets), _ptr(q), num_q_heads, scale, _ptr(out))
         return st, out
+
+    def kv_project(self, seq_ids, x, W_k, W_v, rope_theta=500000.0, rms_eps=1e-5):
+        """(status, K, V) [n, H, D]: the rows' K/V at position lengths[s]."""
+        seq_ids, x = _i32(seq_ids), _f64(x)
+        n, d = x.shape
+        K = np.zeros((n, self.H, self.D))
+        V = np.zeros((n, self.H, self.D))
+        s = self._struct()
+        st = lib().orc_kv_project(C.byref(s), _ptr(seq_ids), n, _ptr(x), d, _ptr(_f64(W_k)), _ptr(_f64(W_v)),
+                                  rope_theta, rms_eps, _ptr(K), _ptr(V))
+        return st, K, V
 
     # logical view helpers (pure indexing, used by tests)
     def logical_kv(self, s):

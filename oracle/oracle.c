@@ -726,3 +726,30 @@ int orc_span_dedupe(const int32_t *span_rule, const int32_t *span_start,
   }
   return U;
 }
+
+/* ------------------------------------------------------------------------ */
+/* The surrogate's K/V state at its compressed position.                    */
+
+int orc_kv_project(const orc_cache *c, const int32_t *seq_ids, int n,
+                   const double *x, int d, const double *W_k,
+                   const double *W_v, double rope_theta, double rms_eps,
+                   double *K, double *V) {
+  const int H = c->num_kv_heads, D = c->head_dim;
+  for (int i = 0; i < n; ++i)
+    if (seq_ids[i] < 0 || seq_ids[i] >= c->max_seqs) return ORC_EINVAL;
+  double *xn = (double *)malloc(sizeof(double) * (size_t)d);
+  for (int i = 0; i < n; ++i) {
+    const double *xi = x + (int64_t)i * d;
+    double ms = 0.0;
+    for (int j = 0; j < d; ++j) ms += xi[j] * xi[j];
+    const double inv = 1.0 / sqrt(ms / d + rms_eps);
+    for (int j = 0; j < d; ++j) xn[j] = xi[j] * inv;
+    double *ki = K + (int64_t)i * H * D, *vi = V + (int64_t)i * H * D;
+    linear(W_k, NULL, xn, d, H * D, ki);
+    linear(W_v, NULL, xn, d, H * D, vi);
+    const double pos = c->lengths[seq_ids[i]];
+    for (int h = 0; h < H; ++h) rope_rotate_half(ki + (int64_t)h * D, D, pos, rope_theta);
+  }
+  free(xn);
+  return ORC_OK;
+}

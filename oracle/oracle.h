@@ -153,6 +153,18 @@ int orc_span_dedupe(const int32_t *span_rule, const int32_t *span_start,
                     int32_t *span_slot, int32_t *uniq_row_idx,
                     int32_t *uniq_span_offsets);
 
+/* The surrogate's single K/V state (appendix "Decoding-time Integration":
+ * the frozen backbone processes z_s as one input embedding; the K/V
+ * append): for request i, the input row x[i] (a surrogate or a plain
+ * token embedding) at the compressed position p = lengths[seq_ids[i]] (the
+ * slot it will take) gives, per kv head, K = RoPE_p(W_k RMSNorm(x)) and
+ * V = W_v RMSNorm(x), the first layer's input side with the norm's gain
+ * folded into W_k, W_v.  K, V: [n][num_kv_heads][head_dim]. */
+int orc_kv_project(const orc_cache *c, const int32_t *seq_ids, int n,
+                   const double *x, int d, const double *W_k,
+                   const double *W_v, double rope_theta, double rms_eps,
+                   double *K, double *V);
+
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int orc_num_threads(void);
 
