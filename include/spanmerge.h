@@ -28,6 +28,9 @@
  *                       the cache crop it implies
  *   sm_gather_surrogates surrogates looked up per rule (or plain token rows)
  *   sm_span_dedupe      one surrogate per distinct rule in a merge batch
+ *   sm_kv_project       the K/V state of an input row (surrogate or token) at
+ *                       its compressed position; sm_kv_append_projected
+ *                       appends it
  *
  * General rules for every call
  * ----------------------------
@@ -498,6 +501,49 @@ sm_status sm_span_dedupe(const int32_t *span_rule, const int32_t *span_start,
                          int32_t *uniq_row_idx, int32_t *uniq_span_offsets,
                          int32_t *num_uniq, void *ws, size_t ws_bytes,
                          int32_t *err, hipStream_t stream);
+
+/*
+ * The K/V state of one input row per request at its compressed position
+ * (appendix "Decoding-time Integration": the frozen backbone processes the
+ * surrogate z_s as one input embedding and produces one K/V state for the
+ * span).  For the first attention layer, with the RMSNorm gain folded into
+ * the projections:
+ *
+ *   K[i, g] = RoPE_p(W_k RMSNorm(x[i]))[g],  V[i, g] = (W_v RMSNorm(x[i]))[g]
+ *   RMSNorm(x) = x / sqrt(mean(x^2) + rms_eps)
+ *   p = lengths[seq_ids[i]] when the call starts (the slot the row takes)
+ *   RoPE_p: rotate-half; pair (j, j + D/2) of each head turned by the angle
+ *           p * rope_theta^(-2j/D)
+ */
+typedef struct {
+  int d;              /* input width: a multiple of 256 */
+  const void *W_k;    /* [num_kv_heads * head_dim][d] bf16, row-major (y = W x) */
+  const void *W_v;    /* [num_kv_heads * head_dim][d] bf16 */
+  float rope_theta;   /* RoPE base, > 0 (Llama 3: 500000) */
+  float rms_eps;      /* >= 0 */
+} sm_kv_proj_params;
+
+/* Workspace of sm_kv_project / sm_kv_append_projected (about
+ * 8 x n x num_kv_heads x head_dim x d / 256 bytes). */
+size_t sm_kv_project_workspace_bytes(int n, int d, int num_kv_heads,
+                                     int head_dim);
+
+/*
+ * sm_kv_project -- K, V [n][num_kv_heads][head_dim] bf16 of the rows
+ * x [n][d] bf16 (the step inputs: sm_gather_surrogates' output), for the
+ * sequences seq_ids [n] of the bf16 cache c (only their lengths are read;
+ * an id outside [0, max_seqs) takes position 0).  n <= min(max_seqs,
+ * SM_MAX_REQUESTS).  K and V can go to sm_decode_step as its new rows.
+ */
+sm_status sm_kv_project(const sm_paged_cache *c, const int32_t *seq_ids, int n,
+                        const void *x, const sm_kv_proj_params *p, void *K,
+                        void *V, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* sm_kv_append_projected -- sm_kv_project, then sm_kv_append of one row per
+ * listed sequence (all of sm_kv_append's checks and errors apply). */
+sm_status sm_kv_append_projected(const sm_paged_cache *c, const int32_t *seq_ids,
+                                 int n, const void *x, const sm_kv_proj_params *p,
+                                 void *ws, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

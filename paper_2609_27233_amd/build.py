@@ -17,7 +17,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libspanmerge.so")
-SOURCES = ["decode_attn.hip", "kv_paged.hip", "lut.hip", "merge_spans.hip", "prefill_attn.hip", "rules.hip"]
+SOURCES = ["decode_attn.hip", "kv_paged.hip", "kvproj.hip", "lut.hip", "merge_spans.hip", "prefill_attn.hip", "rules.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -28,7 +28,8 @@ EXPORTED = ("sm_status_string", "sm_merge_workspace_bytes", "sm_merge_spans",
             "sm_decode_workspace_bytes", "sm_decode_attention", "sm_decode_step",
             "sm_prefill_attention", "sm_rules_build_workspace_bytes", "sm_rules_build",
             "sm_rules_lookup", "sm_match_prompt_workspace_bytes", "sm_match_prompt",
-            "sm_match_decode", "sm_gather_surrogates", "sm_span_dedupe_workspace_bytes", "sm_span_dedupe")
+            "sm_match_decode", "sm_gather_surrogates", "sm_span_dedupe_workspace_bytes", "sm_span_dedupe",
+            "sm_kv_project_workspace_bytes", "sm_kv_project", "sm_kv_append_projected")
 
 
 class MergeParams(C.Structure):
@@ -47,6 +48,10 @@ class PagedCacheDesc(C.Structure):
 
 class RuleTableDesc(C.Structure):
     _fields_ = [("capacity", _I), ("keys", _P), ("ids", _P), ("err", _P)]
+
+
+class KVProjParams(C.Structure):
+    _fields_ = [("d", _I), ("W_k", _P), ("W_v", _P), ("rope_theta", _F), ("rms_eps", _F)]
 
 
 class SpanMergeError(RuntimeError):
@@ -108,6 +113,12 @@ def load(path: str = LIB_PATH):
     L.sm_span_dedupe_workspace_bytes.restype = _Z
     L.sm_span_dedupe.argtypes = [_P, _P, _P, _I, _I, _P, _I, _P, _P, _P, _P, _P, _P, _Z, _P, _P]
     L.sm_span_dedupe.restype = _I
+    L.sm_kv_project_workspace_bytes.argtypes = [_I, _I, _I, _I]
+    L.sm_kv_project_workspace_bytes.restype = _Z
+    L.sm_kv_project.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, C.POINTER(KVProjParams), _P, _P, _P, _Z, _P]
+    L.sm_kv_project.restype = _I
+    L.sm_kv_append_projected.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, C.POINTER(KVProjParams), _P, _Z, _P]
+    L.sm_kv_append_projected.restype = _I
     _lib = L
     return L
 
@@ -356,3 +367,39 @@ def span_dedupe(span_rule, span_start, span_len, num_rules, token_ids, uniq_span
                                _ptr(uniq_span_offsets), _ptr(num_uniq), _ptr(ws), ws.numel() * ws.element_size(),
                                _ptr(err), _stream(stream))
     _check(st, "sm_span_dedupe")
+
+
+# --------------------------------------------------------------------------
+# K/V state of an input row at its compressed position
+
+def _proj_params(W_k, W_v, rope_theta, rms_eps):
+    return KVProjParams(W_k.shape[1], _ptr(W_k), _ptr(W_v), rope_theta, rms_eps)
+
+
+def kv_project_workspace_bytes(n: int, d: int, num_kv_heads: int, head_dim: int) -> int:
+    return load().sm_kv_project_workspace_bytes(n, d, num_kv_heads, head_dim)
+
+
+def kv_project(cache: PagedCache, seq_ids, x, W_k, W_v, K, V, ws=None, rope_theta=500000.0, rms_eps=1e-5,
+               stream=None):
+    """K, V [n, Hkv, D] bf16 of the rows x [n, d] at positions lengths[seq_ids]."""
+    n = seq_ids.numel()
+    if ws is None:
+        ws = torch.empty(kv_project_workspace_bytes(n, x.shape[1], cache.H, cache.D), dtype=torch.uint8,
+                         device=x.device)
+    p = _proj_params(W_k, W_v, rope_theta, rms_eps)
+    st = load().sm_kv_project(C.byref(cache.desc), _ptr(seq_ids), n, _ptr(x), C.byref(p), _ptr(K), _ptr(V),
+                              _ptr(ws), ws.numel() * ws.element_size(), _stream(stream))
+    _check(st, "sm_kv_project")
+
+
+def kv_append_projected(cache: PagedCache, seq_ids, x, W_k, W_v, ws=None, rope_theta=500000.0, rms_eps=1e-5,
+                        stream=None):
+    n = seq_ids.numel()
+    if ws is None:
+        ws = torch.empty(kv_project_workspace_bytes(n, x.shape[1], cache.H, cache.D), dtype=torch.uint8,
+                         device=x.device)
+    p = _proj_params(W_k, W_v, rope_theta, rms_eps)
+    st = load().sm_kv_append_projected(C.byref(cache.desc), _ptr(seq_ids), n, _ptr(x), C.byref(p), _ptr(ws),
+                                       ws.numel() * ws.element_size(), _stream(stream))
+    _check(st, "sm_kv_append_projected")

@@ -171,3 +171,26 @@ def test_lut_call_argument_checks(L):
     assert dd(ws_bytes=need - 1) == sm.SM_EINVAL
     assert dd(S=-1) == sm.SM_EINVAL
     assert dd(rule=None) == sm.SM_EINVAL
+
+
+def test_kv_project_argument_checks(L):
+    d = _desc()
+    p = sm.KVProjParams(4096, 1, 1, 500000.0, 1e-5)
+    need = L.sm_kv_project_workspace_bytes(4, 4096, 8, 128)
+    assert need >= 16 * 4 * 2048 * 4
+    assert L.sm_kv_project_workspace_bytes(4, 4000, 8, 128) == 0               # d not a multiple of 256
+    kp = lambda desc=d, n=4, prm=p, ws_bytes=need, K=1: L.sm_kv_project(C.byref(desc), 1, n, 1, C.byref(prm), K, 1,
+                                                                       1, ws_bytes, None)
+    assert kp(n=0) == sm.SM_OK
+    assert kp(ws_bytes=need - 1) == sm.SM_EINVAL
+    assert kp(n=5) == sm.SM_EINVAL                                             # n > max_seqs (4)
+    assert kp(desc=_desc(dtype=sm.SM_F32)) == sm.SM_EINVAL                     # bf16 caches only
+    assert kp(prm=sm.KVProjParams(4000, 1, 1, 500000.0, 1e-5)) == sm.SM_EINVAL
+    assert kp(prm=sm.KVProjParams(4096, 1, 1, 0.0, 1e-5)) == sm.SM_EINVAL      # theta must be > 0
+    assert kp(prm=sm.KVProjParams(4096, None, 1, 500000.0, 1e-5)) == sm.SM_EINVAL
+    assert kp(K=None) == sm.SM_EINVAL
+    ap = lambda desc=d, n=4, ws_bytes=need: L.sm_kv_append_projected(C.byref(desc), 1, n, 1, C.byref(p), 1,
+                                                                      ws_bytes, None)
+    assert ap(n=0) == sm.SM_OK
+    assert ap(ws_bytes=need - 1) == sm.SM_EINVAL
+    assert ap(desc=_desc(head_dim=96)) == sm.SM_EINVAL
