@@ -395,6 +395,7 @@ def extras_report(job, stream, attn_us):
     out["prefill_attention"] = prefill_report(job.sm, job.L, dev, stream)
     out["rule_matching"] = rules_report(job.sm, job.L, dev, stream)
     out["surrogate_lookup"] = lut_report(job.sm, job.L, dev, stream)
+    out["kv_projection"] = kvproj_report(job.sm, job.L, dev, stream)
     return out
 
 
@@ -631,6 +632,57 @@ def lut_report(sm, L, dev, stream, reps=20):
                 "follow Zipf(1.2) over the rule list"}
 
 
+def kvproj_report(sm, L, dev, stream, reps=50):
+    """The step inputs' K/V states (RMSNorm, W_k / W_v of the Llama-3-8B
+    layer: 1024 x 4096 each, bf16, RoPE at the compressed position) for the
+    16 decode sequences and for the 128 of the Qwen-shaped config, with and
+    without the append."""
+    import torch
+    from paper_2609_27233_amd import workload as wl
+    st = stream.cuda_stream
+    res = {}
+    for wid, name in ((2, "llama3_8b_16_seqs"), (4, "qwen2_7b_128_seqs")):
+        w = wl.WORKLOADS[wid]
+        n, d, H, D = w.batch, w.d, w.num_kv_heads, w.head_dim
+        HD = H * D
+        g = wl.generator(31, dev)
+        x = wl.randn((n, d), torch.bfloat16, g, device=dev)
+        Wk = wl.randn((HD, d), torch.bfloat16, g, device=dev, std=d ** -0.5)
+        Wv = wl.randn((HD, d), torch.bfloat16, g, device=dev, std=d ** -0.5)
+        c = sm.PagedCache(dtype=torch.bfloat16, num_kv_heads=H, head_dim=D, block_size=w.block_size,
+                          num_blocks=n * (reps + 8), max_seqs=n, max_blocks_per_seq=reps + 8, device=dev)
+        ids = torch.arange(n, dtype=torch.int32, device=dev)
+        K = torch.empty((n, H, D), dtype=torch.bfloat16, device=dev)
+        V = torch.empty_like(K)
+        ws = torch.empty(sm.kv_project_workspace_bytes(n, d, H, D), dtype=torch.uint8, device=dev)
+        p = sm.KVProjParams(d, Wk.data_ptr(), Wv.data_ptr(), 500000.0, 1e-5)
+        dsc = C.byref(c.desc)
+
+        def proj():
+            if L.sm_kv_project(dsc, ids.data_ptr(), n, x.data_ptr(), C.byref(p), K.data_ptr(), V.data_ptr(),
+                               ws.data_ptr(), ws.numel(), st):
+                raise RuntimeError("sm_kv_project failed")
+
+        def proj_append():
+            if L.sm_kv_append_projected(dsc, ids.data_ptr(), n, x.data_ptr(), C.byref(p), ws.data_ptr(), ws.numel(),
+                                        st):
+                raise RuntimeError("sm_kv_append_projected failed")
+        t_p = _time(proj, stream, reps)
+        t_a = _time(proj_append, stream, reps)      # appends reps + 1 rows per sequence
+        assert c.error_bits() == 0
+        wbytes = 2 * HD * d * 2
+        byts = wbytes + n * d * 2 + 2 * n * HD * 2
+        res[name] = {"rows": n, "d": d, "kv_features": 2 * HD, "weights_MB": round(wbytes / 1e6, 1),
+                     "project_us": round(t_p * 1e3, 2), "project_GBps": round(byts / (t_p * 1e-3) / 1e9, 1),
+                     "project_frac_of_hbm_peak": round(byts / (t_p * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                     "project_and_append_us": round(t_a * 1e3, 2)}
+        del c, ws
+        torch.cuda.empty_cache()
+    res["note"] = ("HIP events around back-to-back calls; bytes = W_k + W_v + the input rows + the K/V rows; "
+                   "the weights stream from HBM once per call (they do not stay in the 4 MB L2 of an XCD)")
+    return res
+
+
 def traffic_bytes(alg_bytes):
     """Measured HBM bytes per attention launch, or None when the kernel
     sources differ from the ones the counters were taken on."""
@@ -723,6 +775,8 @@ def main():
                     help="only run a plain device copy of BYTES three times (scales HBM counters) and exit")
     ap.add_argument("--merge-only", action="store_true",
                     help="only time the merge module over the 70B-shaped prompt batch and print that")
+    ap.add_argument("--kvproj-only", action="store_true",
+                    help="only time the K/V projection of the step inputs (with and without the append)")
     ap.add_argument("--lut-only", action="store_true",
                     help="only time the surrogate lookup, the merge module on the same spans, and the dedupe")
     ap.add_argument("--rules-only", action="store_true",
@@ -754,6 +808,10 @@ def main():
     if args.merge_only:
         from paper_2609_27233_amd import lib as sm
         print(json.dumps(merge_70b_report(sm, sm.load(), dev, torch.cuda.current_stream(), reps=5)), flush=True)
+        return
+    if args.kvproj_only:
+        from paper_2609_27233_amd import lib as sm
+        print(json.dumps(kvproj_report(sm, sm.load(), dev, torch.cuda.current_stream())), flush=True)
         return
     if args.lut_only:
         from paper_2609_27233_amd import lib as sm

@@ -18,9 +18,10 @@
 //     the d inputs for up to 64 rows (v_mfma_f32_16x16x32_bf16, the rows'
 //     slice staged in LDS, the weight fragments loaded straight into the
 //     operand registers), 256 x d/256 workgroups for d = 4096;
-//  2. one workgroup per row sums the partials in a fixed order (the result
-//     does not depend on scheduling), scales by 1/rms, rotates K by the
-//     position (angles in double precision) and writes bf16 rows;
+//  2. one workgroup per (row, 256 output features) sums the partials in a
+//     fixed order (the result does not depend on scheduling), scales by
+//     1/rms, rotates K by the position (the angle formed and reduced in
+//     double precision, then fp32 sin/cos) and writes bf16 rows;
 //  3. sm_kv_append_projected then appends those rows (block allocation and
 //     all checks of sm_kv_append).
 #include "common.hpp"
@@ -55,7 +56,8 @@ __global__ __launch_bounds__(kPjThreads) void kv_proj_partial_kernel(ProjArgs a)
   for (int s = 0; s < kPjK / 32; ++s)
     wf[s] = __builtin_nontemporal_load((const u32x4_t *)(W + (int64_t)r * a.d + k0 + 32 * s + 8 * q4));
   // the rows' slice k0 .. k0 + 255 into LDS (rows past n are zero)
-  for (int c = tid; c < kPjRows * (kPjK / 8); c += kPjThreads) {
+  const int rows16 = (nr + 15) & ~15;  // whole 16-row tiles
+  for (int c = tid; c < rows16 * (kPjK / 8); c += kPjThreads) {
     const int row = c / (kPjK / 8), ch = c % (kPjK / 8);
     u32x4_t v = u32x4_t{0u, 0u, 0u, 0u};
     if (row < nr) v = *(const u32x4_t *)(a.x + (int64_t)(r0 + row) * a.d + k0 + 8 * ch);
@@ -93,14 +95,19 @@ struct ProjEpiArgs {
   uint16_t *K, *V;        // [n][HD] bf16
   int32_t *row_offsets;   // [n + 1] (nullable)
   int n, d, HD, D, nkc, max_seqs;
-  double rope_theta;
   float rms_eps;
+  double inv_freq[64];    // theta^(-2j/D), j < D/2, computed on the host
 };
 
+constexpr double kTwoPi = 6.283185307179586476925286766559;
+
+// One workgroup per (block of 256 output features, row): a block covers
+// whole heads, so both halves of every rotary pair are at hand.
 __global__ __launch_bounds__(kPjThreads) void kv_proj_epilogue_kernel(ProjEpiArgs a) {
-  __shared__ float ys[2 * 2048];
+  __shared__ float ys[kPjThreads];
   __shared__ float red[16];
-  const int i = blockIdx.x, tid = threadIdx.x;
+  const int fb = blockIdx.x, i = blockIdx.y, tid = threadIdx.x;
+  const int f = fb * kPjThreads + tid;  // K features first, then V
   const int s = a.seq_ids[i];
   const double pos = (s >= 0 && s < a.max_seqs) ? (double)a.lengths[s] : 0.0;  // bad ids fail in the append
   // RMSNorm scale of the row
@@ -112,24 +119,25 @@ __global__ __launch_bounds__(kPjThreads) void kv_proj_epilogue_kernel(ProjEpiArg
   ss = block_sum(ss, red);
   const float inv = rsqrtf(ss / a.d + a.rms_eps);
   // the split-K partials in a fixed order
-  for (int f = tid; f < 2 * a.HD; f += kPjThreads) {
-    float y = 0.f;
-    for (int kc = 0; kc < a.nkc; ++kc) y += a.part[((int64_t)kc * a.n + i) * (2 * a.HD) + f];
-    ys[f] = y * inv;
-  }
+  float y = 0.f;
+  for (int kc = 0; kc < a.nkc; ++kc) y += a.part[((int64_t)kc * a.n + i) * (2 * a.HD) + f];
+  y *= inv;
+  ys[tid] = y;
   __syncthreads();
-  // K: rotate-half RoPE, pair (j, j + D/2) of each head turned by p theta^(-2j/D)
-  const int half = a.D / 2;
-  for (int q = tid; q < a.HD / 2; q += kPjThreads) {
-    const int h = q / half, j = q - h * half;
-    const double ang = pos * pow(a.rope_theta, -2.0 * j / a.D);
-    const float c = (float)cos(ang), sn = (float)sin(ang);
-    const float y1 = ys[h * a.D + j], y2 = ys[h * a.D + j + half];
-    a.K[(int64_t)i * a.HD + h * a.D + j] = f32_to_bf16(y1 * c - y2 * sn);
-    a.K[(int64_t)i * a.HD + h * a.D + j + half] = f32_to_bf16(y2 * c + y1 * sn);
+  if (f < a.HD) {
+    // rotate-half RoPE: pair (j, j + D/2) turned by pos theta^(-2j/D); the
+    // angle is formed and reduced to [-pi, pi] in double precision
+    const int half = a.D / 2, jd = f % a.D, j = jd % half;
+    const double ang = pos * a.inv_freq[j];
+    const float r = (float)(ang - kTwoPi * rint(ang / kTwoPi));
+    const float c = cosf(r), sn = sinf(r);
+    const float other = ys[jd < half ? tid + half : tid - half];
+    const float out = jd < half ? y * c - other * sn : y * c + other * sn;
+    a.K[(int64_t)i * a.HD + f] = f32_to_bf16(out);
+  } else {
+    a.V[(int64_t)i * a.HD + f - a.HD] = f32_to_bf16(y);
   }
-  for (int f = tid; f < a.HD; f += kPjThreads) a.V[(int64_t)i * a.HD + f] = f32_to_bf16(ys[a.HD + f]);
-  if (a.row_offsets && tid == 0) {
+  if (a.row_offsets && fb == 0 && tid == 0) {
     a.row_offsets[i] = i;
     if (i == a.n - 1) a.row_offsets[a.n] = a.n;
   }
@@ -147,7 +155,7 @@ static bool proj_ok(const sm_paged_cache *c, int n, const void *x, const sm_kv_p
   if (!c || !p || n < 0 || n > SM_MAX_REQUESTS || n > c->max_seqs) return false;
   if (c->dtype != SM_BF16 || (c->head_dim != 64 && c->head_dim != 128) || c->num_kv_heads <= 0) return false;
   const int HD = c->num_kv_heads * c->head_dim;
-  if (HD > 2048 || (2 * HD) % kPjFeat != 0) return false;
+  if (HD > 2048 || (2 * HD) % kPjThreads != 0) return false;
   if (p->d <= 0 || p->d % kPjK != 0 || !(p->rope_theta > 0.f) || !(p->rms_eps >= 0.f)) return false;
   return n == 0 || (x && p->W_k && p->W_v && c->lengths);
 }
@@ -166,8 +174,9 @@ static sm_status launch_project(const sm_paged_cache *c, const int32_t *seq_ids,
   const dim3 grid(2 * HD / kPjFeat, p->d / kPjK, (n + kPjRows - 1) / kPjRows);
   hipLaunchKernelGGL(kv_proj_partial_kernel, grid, dim3(kPjThreads), 0, stream, a);
   ProjEpiArgs e{(const uint16_t *)x, part, seq_ids, c->lengths, (uint16_t *)K, (uint16_t *)V, row_offsets,
-                n, p->d, HD, c->head_dim, p->d / kPjK, c->max_seqs, (double)p->rope_theta, p->rms_eps};
-  hipLaunchKernelGGL(kv_proj_epilogue_kernel, dim3(n), dim3(kPjThreads), 0, stream, e);
+                n, p->d, HD, c->head_dim, p->d / kPjK, c->max_seqs, p->rms_eps, {}};
+  for (int j = 0; j < c->head_dim / 2; ++j) e.inv_freq[j] = pow((double)p->rope_theta, -2.0 * j / c->head_dim);
+  hipLaunchKernelGGL(kv_proj_epilogue_kernel, dim3(2 * HD / kPjThreads, n), dim3(kPjThreads), 0, stream, e);
   return hipGetLastError() == hipSuccess ? SM_OK : SM_EHIP;
 }
 
