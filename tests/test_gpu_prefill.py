@@ -150,3 +150,44 @@ def test_llama3_8b_prompt_batch_sampled(orc):
     e_head = rel_l2_max(out[first], ref2)
     say("rel_l2_max last rows", e_tail, "first rows", e_head)
     assert e_tail <= TOL[torch.bfloat16] and e_head <= TOL[torch.bfloat16]
+
+
+@pytest.mark.parametrize("wid", [3, 5])
+def test_prompt_batch_full_size_sampled(orc, wid):
+    """The compressed prompt batches of the long-context config (4 x 19661
+    positions over shuffled pages) and of the 70B-shaped config (32 x 4915
+    positions, 64 query heads, group 8) at full size; checked on the last 4
+    rows of every request and the first 24 rows of one."""
+    w = wl.WORKLOADS[wid]
+    Hq, H, D, bs = w.num_q_heads, w.num_kv_heads, w.head_dim, w.block_size
+    L0 = w.prompt_len - int(round(w.target * w.prompt_len))
+    rng = np.random.RandomState(40 + wid)
+    lens = [L0] * w.batch
+    oc, c = _cache(orc, rng, H, D, bs, lens)
+    ids = np.arange(w.batch, dtype=np.int32)
+    qo = np.arange(w.batch + 1, dtype=np.int32) * L0
+    gq = wl.generator(50 + wid, "cuda")
+    q = wl.randn((int(qo[-1]), Hq, D), torch.bfloat16, gq, device="cuda")
+    out = torch.full(q.shape, float("nan"), dtype=torch.bfloat16, device=dev())
+    say("prefill config", wid, w.batch, "x", L0)
+    sm.prefill_attention(c, i32(ids), i32(qo), q, out, L0)
+    torch.cuda.synchronize()
+    assert c.error_bits() == 0
+    k = 4
+    rows = np.concatenate([np.arange(qo[i + 1] - k, qo[i + 1]) for i in range(w.batch)])
+    rows_t = torch.as_tensor(rows, device=dev())
+    st, ref = oc.prefill_attention(ids, np.arange(w.batch + 1, dtype=np.int32) * k,
+                                   wl.to_f64(q[rows_t].cpu()), Hq, D ** -0.5)
+    assert st == orc.OK
+    e_tail = rel_l2_max(out[rows_t].float().cpu().numpy(), ref)
+    head = orc.OracleCache(bf16=True, num_kv_heads=H, head_dim=D, block_size=bs, num_blocks=oc.num_blocks,
+                           max_seqs=oc.max_seqs, max_blocks_per_seq=oc.max_blocks)
+    head.k_pool[:], head.v_pool[:], head.block_table[:] = oc.k_pool, oc.v_pool, oc.block_table
+    head.lengths[:] = 0
+    head.lengths[1] = 24
+    first = torch.arange(int(qo[1]), int(qo[1]) + 24, device=dev())
+    st, ref2 = head.prefill_attention([1], [0, 24], wl.to_f64(q[first].cpu()), Hq, D ** -0.5)
+    assert st == orc.OK
+    e_head = rel_l2_max(out[first].float().cpu().numpy(), ref2)
+    say("rel_l2_max last rows", e_tail, "first rows", e_head)
+    assert e_tail <= TOL[torch.bfloat16] and e_head <= TOL[torch.bfloat16]

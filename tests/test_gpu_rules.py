@@ -204,3 +204,20 @@ def test_match_decode_repeated_id_changes_nothing(orc):
     torch.cuda.synchronize()
     assert t.error_bits() == sm.ERR_EINVAL
     assert torch.equal(state, before) and k_out.cpu().tolist() == [0, 0] and r_out.cpu().tolist() == [-1, -1]
+
+
+@pytest.mark.parametrize("B,T", [(4, 32768), (32, 8192)])
+def test_match_prompt_long_and_wide_batches(orc, B, T):
+    """The prompt shapes of the long-context (4 x 32768: eight scan passes
+    per sequence) and 70B-shaped (32 x 8192) configs, 2.17M rules."""
+    rules = wl.make_rules()
+    toks, offs = wl.make_rule_prompts(rules, B, T, 0.4, 128256, seed=B)
+    R = orc.OracleRules(rules)
+    st, s0, ln, ru, sso = R.match_prompt(toks, offs)
+    assert st == orc.OK
+    t = _table(rules)
+    say("match_prompt", B, "x", T, "spans", len(s0))
+    g0, gl, gr, gs = _gpu_match(t, toks, offs)
+    assert t.error_bits() == 0
+    assert np.array_equal(gs, sso)
+    assert np.array_equal(g0, s0) and np.array_equal(gl, ln) and np.array_equal(gr, ru)
