@@ -516,7 +516,7 @@ sm_status sm_span_dedupe(const int32_t *span_rule, const int32_t *span_start,
  *           p * rope_theta^(-2j/D)
  */
 typedef struct {
-  int d;              /* input width: a multiple of 256 */
+  int d;              /* input width: a multiple of 256, at most 16384 */
   const void *W_k;    /* [num_kv_heads * head_dim][d] bf16, row-major (y = W x) */
   const void *W_v;    /* [num_kv_heads * head_dim][d] bf16 */
   float rope_theta;   /* RoPE base, > 0 (Llama 3: 500000) */
@@ -533,8 +533,8 @@ size_t sm_kv_project_workspace_bytes(int n, int d, int num_kv_heads,
  * x [n][d] bf16 (the step inputs: sm_gather_surrogates' output), for the
  * sequences seq_ids [n] of the bf16 cache c (only their lengths are read;
  * an id outside [0, max_seqs) takes position 0).  n <= min(max_seqs,
- * SM_MAX_REQUESTS); num_kv_heads x head_dim a multiple of 128.  K and V can
- * go to sm_decode_step as its new rows.
+ * SM_MAX_REQUESTS); num_kv_heads x head_dim a multiple of 128; x, W_k and
+ * W_v 16-byte aligned.  K and V can go to sm_decode_step as its new rows.
  */
 sm_status sm_kv_project(const sm_paged_cache *c, const int32_t *seq_ids, int n,
                         const void *x, const sm_kv_proj_params *p, void *K,

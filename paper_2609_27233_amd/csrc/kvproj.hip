@@ -32,6 +32,7 @@ constexpr int kPjThreads = 256;
 constexpr int kPjRows = 64;   // rows per workgroup
 constexpr int kPjFeat = 64;   // output features per workgroup, 16 per wave
 constexpr int kPjK = 256;     // inputs per workgroup
+constexpr int kPjMaxChunks = 64;  // d <= 64 x 256
 
 struct ProjArgs {
   const uint16_t *x;   // [n][d]
@@ -110,17 +111,26 @@ __global__ __launch_bounds__(kPjThreads) void kv_proj_epilogue_kernel(ProjEpiArg
   const int f = fb * kPjThreads + tid;  // K features first, then V
   const int s = a.seq_ids[i];
   const double pos = (s >= 0 && s < a.max_seqs) ? (double)a.lengths[s] : 0.0;  // bad ids fail in the append
-  // RMSNorm scale of the row
+  // the split-K partials, summed in a fixed order once all are loaded; their
+  // loads are in flight while the row's RMSNorm scale is reduced
+  float pv[kPjMaxChunks];
+#pragma unroll
+  for (int kc = 0; kc < kPjMaxChunks; ++kc)
+    pv[kc] = kc < a.nkc ? a.part[((int64_t)kc * a.n + i) * (2 * a.HD) + f] : 0.f;
   float ss = 0.f;
-  for (int k = tid; k < a.d; k += kPjThreads) {
-    const float v = bf16_to_f32(a.x[(int64_t)i * a.d + k]);
-    ss += v * v;
+  for (int k = 8 * tid; k < a.d; k += 8 * kPjThreads) {
+    const u32x4_t v = *(const u32x4_t *)(a.x + (int64_t)i * a.d + k);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = __uint_as_float(v[e] << 16), hi = __uint_as_float(v[e] & 0xffff0000u);
+      ss += lo * lo + hi * hi;
+    }
   }
   ss = block_sum(ss, red);
   const float inv = rsqrtf(ss / a.d + a.rms_eps);
-  // the split-K partials in a fixed order
   float y = 0.f;
-  for (int kc = 0; kc < a.nkc; ++kc) y += a.part[((int64_t)kc * a.n + i) * (2 * a.HD) + f];
+#pragma unroll
+  for (int kc = 0; kc < kPjMaxChunks; ++kc) y += pv[kc];
   y *= inv;
   ys[tid] = y;
   __syncthreads();
@@ -156,12 +166,15 @@ static bool proj_ok(const sm_paged_cache *c, int n, const void *x, const sm_kv_p
   if (c->dtype != SM_BF16 || (c->head_dim != 64 && c->head_dim != 128) || c->num_kv_heads <= 0) return false;
   const int HD = c->num_kv_heads * c->head_dim;
   if (HD > 2048 || (2 * HD) % kPjThreads != 0) return false;
-  if (p->d <= 0 || p->d % kPjK != 0 || !(p->rope_theta > 0.f) || !(p->rms_eps >= 0.f)) return false;
+  if (p->d <= 0 || p->d % kPjK != 0 || p->d > kPjK * kPjMaxChunks || !(p->rope_theta > 0.f) ||
+      !(p->rms_eps >= 0.f))
+    return false;
   return n == 0 || (x && p->W_k && p->W_v && c->lengths);
 }
 
 SM_API size_t sm_kv_project_workspace_bytes(int n, int d, int num_kv_heads, int head_dim) {
-  if (n < 0 || d <= 0 || d % kPjK != 0 || num_kv_heads <= 0 || head_dim <= 0) return 0;
+  if (n < 0 || d <= 0 || d % kPjK != 0 || d > kPjK * kPjMaxChunks || num_kv_heads <= 0 || head_dim <= 0)
+    return 0;
   const int HD = num_kv_heads * head_dim;
   return part_bytes(n, d, HD) + 2 * align256((size_t)n * HD * 2) + align256((size_t)(n + 1) * 4);
 }
