@@ -55,7 +55,7 @@ def log(*a):
 class Job:
     """Device state of R resident batches of one workload."""
 
-    def __init__(self, w, R, dev, seed_base=0):
+    def __init__(self, w, R, dev, seed_base=0, token_table=True):
         import torch
         from paper_2609_27233_amd import lib as sm
         from paper_2609_27233_amd import workload as wl
@@ -138,6 +138,21 @@ class Job:
         self.upd_done = [torch.cuda.Event() for _ in range(R)]
         torch.cuda.synchronize()
         self._prep_ctypes()
+        # the merge module's first stage for every vocabulary row, built once
+        # (as at model load) when the job uses the token table
+        self.table, self.table_ms = None, None
+        if token_table:
+            self.table = torch.empty_like(self.emb)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            rc = self.L.sm_merge_token_table(self.emb.data_ptr(), self.emb.shape[0], C.byref(self.mp), sm.SM_BF16,
+                                             self.table.data_ptr(), self.err.data_ptr(),
+                                             torch.cuda.current_stream().cuda_stream)
+            e1.record()
+            torch.cuda.synchronize()
+            if rc or int(self.err.item()):
+                raise RuntimeError(f"sm_merge_token_table failed: {rc}")
+            self.table_ms = e0.elapsed_time(e1)
         log(f"setup {time.time() - t0:.1f}s: R={R}, spans/batch={Smax}, packed rows/batch={self.packed_rows[0]}, "
             f"L0={self.L0}, max_len={self.max_len}")
 
@@ -164,6 +179,17 @@ class Job:
         bt = 4 * int(np.sum(-(-lens // w.block_size)))
         return kv + new_rows + qo + bt
 
+    def _merge_call(self, row_idx, rows, offs, S, z, ws, st):
+        """M_phi over one CSR batch of spans: from the token table when the
+        job has one, else from the embeddings."""
+        L, bf = self.L, self.sm.SM_BF16
+        if self.table is not None:
+            return L.sm_merge_spans_tabled(self.table.data_ptr(), self.table.shape[0], row_idx, rows, offs, S,
+                                           C.byref(self.mp), bf, z, ws.data_ptr(), ws.numel(),
+                                           self.err.data_ptr(), st)
+        return L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], row_idx, rows, offs, S,
+                                C.byref(self.mp), bf, z, ws.data_ptr(), ws.numel(), self.err.data_ptr(), st)
+
     def _merge(self, r, s, st):
         """Decode-time merge of batch r before decode step s: the merge
         module on each sequence's freshly completed span and the roll back of
@@ -171,9 +197,8 @@ class Job:
         L, w = self.L, self.w
         B, bf = w.batch, self.sm.SM_BF16
         m = self.dmerge[s]
-        rc = L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], m["row_idx"].data_ptr(), m["rows"],
-                              m["offs"].data_ptr(), B, C.byref(self.mp), bf, self.zdec.data_ptr(),
-                              self.dmerge_ws.data_ptr(), self.dmerge_ws.numel(), self.err.data_ptr(), st)
+        rc = self._merge_call(m["row_idx"].data_ptr(), m["rows"], m["offs"].data_ptr(), B, self.zdec.data_ptr(),
+                              self.dmerge_ws, st)
         rc |= L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), m["k"].data_ptr(), B, st)
         if rc:
             raise RuntimeError(f"decode-time merge launch failed at step {s}: {rc}")
@@ -212,10 +237,8 @@ class Job:
             with torch.cuda.stream(upd_stream):
                 self.kreset.copy_(c.lengths[:B])   # evict the previous job's sequences
             rc = L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), self.kreset.data_ptr(), B, sb)
-            rc |= L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], dp["row_idx"].data_ptr(), dp["rows"],
-                                   dp["span_offsets"].data_ptr(), dp["S"], C.byref(self.mp), bf,
-                                   self.z.data_ptr(), self.merge_ws.data_ptr(), self.merge_ws.numel(),
-                                   self.err.data_ptr(), sb)
+            rc |= self._merge_call(dp["row_idx"].data_ptr(), dp["rows"], dp["span_offsets"].data_ptr(), dp["S"],
+                                   self.z.data_ptr(), self.merge_ws, sb)
             rc |= L.sm_pack_spans(B, dp["seq_offsets"].data_ptr(), B * w.prompt_len, dp["S"],
                                   dp["span_start"].data_ptr(), dp["span_len"].data_ptr(),
                                   dp["seq_span_offsets"].data_ptr(), self.pi.data_ptr(), self.po.data_ptr(),
@@ -429,10 +452,42 @@ def merge_70b_report(sm, L, dev, stream, reps=3):
     t5 = _time(merge5, stream, reps)
     flop5 = 2.0 * w5.d * w5.d * (R5 + S5)
     assert int(err.item()) == 0
+    # the same surrogates from the token table: the table (vocab x d) is one
+    # GEMM, built once; each call then runs the span-level stages only
+    z5t = torch.empty_like(z5)
+    table5 = torch.empty_like(emb5)
+
+    def table_build():
+        rc = L.sm_merge_token_table(emb5.data_ptr(), emb5.shape[0], C.byref(mp5), sm.SM_BF16, table5.data_ptr(),
+                                    err.data_ptr(), st)
+        if rc:
+            raise RuntimeError(f"sm_merge_token_table failed: {rc}")
+
+    def merge5t():
+        rc = L.sm_merge_spans_tabled(table5.data_ptr(), table5.shape[0], ri.data_ptr(), R5, so.data_ptr(), S5,
+                                     C.byref(mp5), sm.SM_BF16, z5t.data_ptr(), ws5.data_ptr(), ws5.numel(),
+                                     err.data_ptr(), st)
+        if rc:
+            raise RuntimeError(f"sm_merge_spans_tabled failed: {rc}")
+    tb = _time(table_build, stream, 2)
+    tt = _time(merge5t, stream, reps)
+    assert int(err.item()) == 0
+    flop_tb = 2.0 * w5.d * w5.d * emb5.shape[0]
+    flop_t = 2.0 * w5.d * w5.d * S5
+    agree = float((z5t.float() - z5.float()).norm(dim=1).div(z5.float().norm(dim=1)).max())
+    del table5
     return {
         "spans": S5, "rows": R5, "d": w5.d, "ms": round(t5, 3),
         "TFLOPs": round(flop5 / (t5 * 1e-3) / 1e12, 1),
         "frac_of_bf16_peak": round(flop5 / (t5 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "token_table": {
+            "build_ms": round(tb, 3), "build_TFLOPs": round(flop_tb / (tb * 1e-3) / 1e12, 1),
+            "table_GB": round(emb5.numel() * 2 / 1e9, 2),
+            "tabled_merge_ms": round(tt, 3), "tabled_speedup": round(t5 / tt, 2),
+            "tabled_TFLOPs_second_projection": round(flop_t / (tt * 1e-3) / 1e12, 1),
+            "max_rel_l2_vs_direct": round(agree, 5),
+            "note": "sm_merge_token_table over the 128256-row vocabulary, once; sm_merge_spans_tabled over the "
+                    "same spans reads the first stage by token id"},
         "note": "one sm_merge_spans call over every span of the 32 x 8192 prompts; FLOP = 2 d^2 (rows + spans) "
                 "for the two projections (pooling and LayerNorm are O(d) per row)"}
 
@@ -783,6 +838,8 @@ def main():
                     help="only time the rule table build and the prompt / decode matching")
     ap.add_argument("--prefill-only", action="store_true",
                     help="only time the prefill attention over the compacted and uncompressed prompt batch")
+    ap.add_argument("--no-token-table", action="store_true",
+                    help="run the job's merges from the embeddings (sm_merge_spans) instead of the token table")
     ap.add_argument("--overlap", action="store_true",
                     help="run cache updates on a second stream, overlapped with other batches' attention")
     args = ap.parse_args()
@@ -828,7 +885,7 @@ def main():
     w = wl.WORKLOADS[2]
     if args.decode_steps is not None:
         w = dataclasses.replace(w, decode_steps=args.decode_steps)
-    job = Job(w, args.replicas, dev)
+    job = Job(w, args.replicas, dev, token_table=not args.no_token_table)
     stream = torch.cuda.current_stream()
     upd_stream = torch.cuda.Stream() if args.overlap else stream  # default priority
     nlaunch = w.decode_steps * job.R
@@ -879,6 +936,8 @@ def main():
             "batch": w.batch, "prompt_len": w.prompt_len, "compacted_len": job.L0,
             "decode_steps": w.decode_steps, "resident_batches": job.R,
             "update_overlap": bool(args.overlap),
+            "merge_first_stage": ("token table (sm_merge_token_table once, %.2f ms; sm_merge_spans_tabled per call)"
+                                  % job.table_ms) if job.table is not None else "per call (sm_merge_spans)",
             "layer": {"d": w.d, "q_heads": w.num_q_heads, "kv_heads": w.num_kv_heads, "head_dim": w.head_dim},
             "block_size": w.block_size,
         },

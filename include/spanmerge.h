@@ -171,8 +171,8 @@ size_t sm_merge_workspace_bytes(int total_rows, int num_spans, int d,
  *  out           [num_spans][d] surrogates (dtype dt)
  *  ws, ws_bytes  workspace of at least sm_merge_workspace_bytes(...) bytes
  *  err           [1] device error word: EINVAL when a row index is outside
- *                [0, emb_rows) or the span offsets are not a valid CSR
- *                (the affected surrogates are then zero)
+ *                [0, emb_rows) (that row is read as row 0) or the span
+ *                offsets are not a valid CSR (those surrogates are zero)
  */
 sm_status sm_merge_spans(const void *emb, int64_t emb_rows,
                          const int32_t *row_idx, int total_rows,
@@ -180,6 +180,46 @@ sm_status sm_merge_spans(const void *emb, int64_t emb_rows,
                          const sm_merge_params *p, sm_dtype dt, void *out,
                          void *ws, size_t ws_bytes, int32_t *err,
                          hipStream_t stream);
+
+/*
+ * sm_merge_token_table -- the first stage of M_phi for every row of the
+ * embedding table, once (appendix "Attention-based Pooling Architecture":
+ * Linear_kv and GELU act on each static token embedding on its own, so
+ * their output depends on the token alone -- the same context
+ * independence "Computational Scope" notes for whole surrogates):
+ *
+ *   table[v] = GELU(Linear_kv(emb[v]))     v = 0 .. emb_rows - 1
+ *
+ *  emb       [emb_rows][d] static embedding table (dtype dt), emb_rows < 2^31
+ *  p         (host) the merge parameters (only W_kv, b_kv are read; all
+ *            must be set, as for sm_merge_spans)
+ *  table     [emb_rows][d] output (dtype dt), caller-owned
+ *  err       [1] device error word (no device errors are raised)
+ * No workspace.  One GEMM on the matrix cores; it is the cost of
+ * sm_merge_spans's first projection for emb_rows rows.
+ */
+sm_status sm_merge_token_table(const void *emb, int64_t emb_rows,
+                               const sm_merge_params *p, sm_dtype dt,
+                               void *table, int32_t *err, hipStream_t stream);
+
+/*
+ * sm_merge_spans_tabled -- the same surrogates as sm_merge_spans, with the
+ * first stage read from a table made by sm_merge_token_table (LN_kv, the
+ * pooling, Linear_o, GELU and LN_o run per call):
+ *
+ *  table, table_rows  [table_rows][d] rows GELU(Linear_kv(emb[v]))
+ *  row_idx, total_rows, span_offsets, num_spans, p, dt, out, err:
+ *            as sm_merge_spans (row_idx holds token ids, i.e. table rows)
+ *  ws, ws_bytes  workspace of at least
+ *                sm_merge_workspace_bytes(0, num_spans, d, dt) bytes
+ * Device errors: as sm_merge_spans, with table_rows in place of emb_rows.
+ */
+sm_status sm_merge_spans_tabled(const void *table, int64_t table_rows,
+                                const int32_t *row_idx, int total_rows,
+                                const int32_t *span_offsets, int num_spans,
+                                const sm_merge_params *p, sm_dtype dt,
+                                void *out, void *ws, size_t ws_bytes,
+                                int32_t *err, hipStream_t stream);
 
 /*
  * sm_pack_spans -- prompt compression bookkeeping (appendix "Prompt-time

@@ -581,8 +581,27 @@ __device__ __forceinline__ void store_vec(T *p, const float *x) {
   *(u32x4_t *)p = u;
 }
 
+// Row r of the first stage's output: row r of G1, or, with a token table,
+// table row gidx[r] (an index outside [0, g_rows) reads row 0 and sets
+// EINVAL).
+template <typename T>
+__device__ __forceinline__ const T *g1_row(const T *G1, const int32_t *gidx, int64_t g_rows, int r, int d,
+                                           int32_t *err) {
+  int64_t gr = r;
+  if (gidx) {
+    int v = gidx[r];
+    if (v < 0 || v >= g_rows) {
+      set_err(err, SM_ERR_EINVAL);
+      v = 0;
+    }
+    gr = v;
+  }
+  return G1 + gr * d;
+}
+
 template <typename T>
 __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const T *__restrict__ G1,
+                                                            const int32_t *__restrict__ gidx, int64_t g_rows,
                                                             const int32_t *__restrict__ span_offsets,
                                                             int num_spans, int total_rows,
                                                             const T *__restrict__ Q, const T *__restrict__ g_kv,
@@ -625,7 +644,7 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const T *__restrict_
 
   // pass 1: LN statistics and head scores of every row
   for (int j = 0; j < n; ++j) {
-    const T *row = G1 + (int64_t)(r0 + j) * d;
+    const T *row = g1_row(G1, gidx, g_rows, r0 + j, d, err);
     float x[kMaxVec][VN];
     float sum = 0.f;
 #pragma unroll
@@ -703,7 +722,7 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const T *__restrict_
 #pragma unroll
     for (int e = 0; e < VN; ++e) cacc[u][e] = 0.f;
   for (int j = 0; j < n; ++j) {
-    const T *row = G1 + (int64_t)(r0 + j) * d;
+    const T *row = g1_row(G1, gidx, g_rows, r0 + j, d, err);
     const float mean = row_mean[j], inv = row_inv[j];
 #pragma unroll
     for (int u = 0; u < kMaxVec; ++u) {
@@ -735,6 +754,8 @@ constexpr int kPoolWaves = 4;
 
 template <typename T, int NCH>
 __global__ __launch_bounds__(kPoolWaves * 64) void pool_rows_kernel(const T *__restrict__ G1,
+                                                                    const int32_t *__restrict__ gidx,
+                                                                    int64_t g_rows,
                                                                     const int32_t *__restrict__ span_offsets,
                                                                     int num_spans, int total_rows,
                                                                     const T *__restrict__ Q,
@@ -765,7 +786,7 @@ __global__ __launch_bounds__(kPoolWaves * 64) void pool_rows_kernel(const T *__r
   // this wave's first row is requested before the parameters are staged
   u32x4_t xr[NCH];
   if (w < n) {
-    const u32x4_t *row = (const u32x4_t *)(G1 + (int64_t)(r0 + w) * d);
+    const u32x4_t *row = (const u32x4_t *)g1_row(G1, gidx, g_rows, r0 + w, d, err);
 #pragma unroll
     for (int u = 0; u < NCH; ++u) xr[u] = row[u * 64 + lane];
   }
@@ -784,7 +805,7 @@ __global__ __launch_bounds__(kPoolWaves * 64) void pool_rows_kernel(const T *__r
     // hold 3 * NCH * VN floats live across it
     asm volatile("" ::: "memory");
     if (j != w) {
-      const u32x4_t *row = (const u32x4_t *)(G1 + (int64_t)(r0 + j) * d);
+      const u32x4_t *row = (const u32x4_t *)g1_row(G1, gidx, g_rows, r0 + j, d, err);
 #pragma unroll
       for (int u = 0; u < NCH; ++u) xr[u] = row[u * 64 + lane];
     }
@@ -856,7 +877,7 @@ __global__ __launch_bounds__(kPoolWaves * 64) void pool_rows_kernel(const T *__r
       u32x4_t xq[4];
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj)
-        if (j0 + jj < n) xq[jj] = *(const u32x4_t *)(G1 + (int64_t)(r0 + j0 + jj) * d + col);
+        if (j0 + jj < n) xq[jj] = *(const u32x4_t *)(g1_row(G1, gidx, g_rows, r0 + j0 + jj, d, err) + col);
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj)
         if (j0 + jj < n) {
@@ -872,23 +893,23 @@ __global__ __launch_bounds__(kPoolWaves * 64) void pool_rows_kernel(const T *__r
 }
 
 template <typename T>
-static hipError_t launch_pool(const T *G1, const int32_t *span_offsets, int num_spans, int total_rows, const T *Q,
-                              const T *g_kv, const T *beta_kv, float eps, int d, int h, T *cout, int32_t *err,
-                              hipStream_t stream) {
+static hipError_t launch_pool(const T *G1, const int32_t *gidx, int64_t g_rows, const int32_t *span_offsets,
+                              int num_spans, int total_rows, const T *Q, const T *g_kv, const T *beta_kv, float eps,
+                              int d, int h, T *cout, int32_t *err, hipStream_t stream) {
   constexpr int VN = Vec<T>::N;
   const int nch = d % (64 * VN) == 0 ? d / (64 * VN) : 0;
 #define SM_POOL_CASE(C)                                                                                          \
   case C:                                                                                                        \
-    hipLaunchKernelGGL((pool_rows_kernel<T, C>), dim3(num_spans), dim3(kPoolWaves * 64), 0, stream, G1,          \
-                       span_offsets, num_spans, total_rows, Q, g_kv, beta_kv, eps, d, h, cout, err);             \
+    hipLaunchKernelGGL((pool_rows_kernel<T, C>), dim3(num_spans), dim3(kPoolWaves * 64), 0, stream, G1, gidx,    \
+                       g_rows, span_offsets, num_spans, total_rows, Q, g_kv, beta_kv, eps, d, h, cout, err);     \
     break;
   switch (nch) {
     SM_POOL_CASE(1) SM_POOL_CASE(2) SM_POOL_CASE(3) SM_POOL_CASE(4)
     SM_POOL_CASE(5) SM_POOL_CASE(6) SM_POOL_CASE(7) SM_POOL_CASE(8)
     SM_POOL_CASE(16)
     default:
-      hipLaunchKernelGGL(pool_kernel<T>, dim3(num_spans), dim3(kPoolThreads), 0, stream, G1, span_offsets,
-                         num_spans, total_rows, Q, g_kv, beta_kv, eps, d, h, cout, err);
+      hipLaunchKernelGGL(pool_kernel<T>, dim3(num_spans), dim3(kPoolThreads), 0, stream, G1, gidx, g_rows,
+                         span_offsets, num_spans, total_rows, Q, g_kv, beta_kv, eps, d, h, cout, err);
   }
 #undef SM_POOL_CASE
   return hipGetLastError();
@@ -969,47 +990,52 @@ SM_API size_t sm_merge_workspace_bytes(int total_rows, int num_spans, int d, sm_
          align256((size_t)num_spans * d * 4);
 }
 
-SM_API sm_status sm_merge_spans(const void *emb, int64_t emb_rows, const int32_t *row_idx, int total_rows,
-                                const int32_t *span_offsets, int num_spans, const sm_merge_params *p,
-                                sm_dtype dt, void *out, void *ws, size_t ws_bytes, int32_t *err,
-                                hipStream_t stream) {
-  if (!p || total_rows < 0 || num_spans < 0) return SM_EINVAL;
+// Argument checks shared by the merge entry points.
+static sm_status merge_param_check(const sm_merge_params *p, sm_dtype dt) {
+  if (!p) return SM_EINVAL;
   if (dt != SM_F32 && dt != SM_BF16) return SM_EINVAL;
   const int d = p->d, h = p->h;
   if (d <= 0 || d > kMaxD || d % 256 != 0 || h <= 0 || h > kMaxHeads || d % h != 0 || (d / h) % 64 != 0)
     return SM_EINVAL;
-  if (num_spans == 0) return total_rows == 0 ? SM_OK : SM_EINVAL;
-  if (total_rows < num_spans) return SM_EINVAL;
-  if (!emb || emb_rows <= 0 || !row_idx || !span_offsets || !out || !ws || !err) return SM_EINVAL;
-  if (!p->Q || !p->W_kv || !p->b_kv || !p->g_kv || !p->beta_kv || !p->W_o || !p->b_o || !p->g_o ||
-      !p->beta_o)
+  if (!p->Q || !p->W_kv || !p->b_kv || !p->g_kv || !p->beta_kv || !p->W_o || !p->b_o || !p->g_o || !p->beta_o)
     return SM_EINVAL;
-  if (ws_bytes < sm_merge_workspace_bytes(total_rows, num_spans, d, dt)) return SM_EINVAL;
-  if ((total_rows + kBM - 1) / kBM > 65535 || (num_spans + kBM - 1) / kBM > 65535) return SM_EINVAL;
+  return SM_OK;
+}
 
-  const size_t es = dt == SM_BF16 ? 2 : 4;
-  char *wsb = (char *)ws;
-  void *g1 = wsb;
-  void *cbuf = wsb + align256((size_t)total_rows * d * es);
-  float *ybuf = (float *)(wsb + align256((size_t)total_rows * d * es) + align256((size_t)num_spans * d * es));
-
+// First stage: C[M][d] = GELU(A[rows][d] W_kv^T + b_kv), the A rows gathered
+// through `gather` when given (else rows 0 .. M-1).
+static sm_status first_stage(const void *A, const int32_t *gather, int64_t a_rows, int M, const sm_merge_params *p,
+                             sm_dtype dt, void *C, int32_t *err, hipStream_t stream) {
+  const int d = p->d;
   if (dt == SM_BF16) {
-    if (total_rows <= kSkinnyMaxM)
-      launch_skinny<uint16_t>((const uint16_t *)emb, row_idx, emb_rows, (const uint16_t *)p->W_kv,
-                              (const uint16_t *)p->b_kv, (uint16_t *)g1, total_rows, d, d, err, stream);
-    else if (use_gemm256(total_rows, d, d)) {
-      if (launch_gemm256<uint16_t>((const uint16_t *)emb, row_idx, emb_rows, (const uint16_t *)p->W_kv,
-                                   (const uint16_t *)p->b_kv, (uint16_t *)g1, total_rows, d, d, err,
-                                   stream) != hipSuccess)
+    if (M <= kSkinnyMaxM)
+      launch_skinny<uint16_t>((const uint16_t *)A, gather, a_rows, (const uint16_t *)p->W_kv,
+                              (const uint16_t *)p->b_kv, (uint16_t *)C, M, d, d, err, stream);
+    else if (use_gemm256(M, d, d)) {
+      if (launch_gemm256<uint16_t>((const uint16_t *)A, gather, a_rows, (const uint16_t *)p->W_kv,
+                                   (const uint16_t *)p->b_kv, (uint16_t *)C, M, d, d, err, stream) != hipSuccess)
         return SM_EHIP;
     } else
-      hipLaunchKernelGGL(gemm_bf16_nt_gelu<uint16_t>, dim3(d / kBN, (total_rows + kBM - 1) / kBM), dim3(256), 0,
-                         stream, (const uint16_t *)emb, row_idx, emb_rows, (const uint16_t *)p->W_kv,
-                         (const uint16_t *)p->b_kv, (uint16_t *)g1, total_rows, d, d, err);
-    if (hipGetLastError() != hipSuccess) return SM_EHIP;
-    if (launch_pool<uint16_t>((const uint16_t *)g1, span_offsets, num_spans, total_rows, (const uint16_t *)p->Q,
-                              (const uint16_t *)p->g_kv, (const uint16_t *)p->beta_kv, p->ln_eps, d, h,
-                              (uint16_t *)cbuf, err, stream) != hipSuccess)
+      hipLaunchKernelGGL(gemm_bf16_nt_gelu<uint16_t>, dim3(d / kBN, (M + kBM - 1) / kBM), dim3(256), 0, stream,
+                         (const uint16_t *)A, gather, a_rows, (const uint16_t *)p->W_kv, (const uint16_t *)p->b_kv,
+                         (uint16_t *)C, M, d, d, err);
+  } else {
+    hipLaunchKernelGGL(gemm_f32_nt_gelu, dim3(d / kFT, (M + kFT - 1) / kFT), dim3(256), 0, stream, (const float *)A,
+                       gather, a_rows, (const float *)p->W_kv, (const float *)p->b_kv, (float *)C, M, d, d, err);
+  }
+  return hipGetLastError() == hipSuccess ? SM_OK : SM_EHIP;
+}
+
+// Pooling, second projection and LN_o over the first-stage rows G1 (row r
+// of the CSR list is G1 row gidx[r] when gidx is given, else row r).
+static sm_status pool_and_project(const void *G1, const int32_t *gidx, int64_t g_rows, int total_rows,
+                                  const int32_t *span_offsets, int num_spans, const sm_merge_params *p, sm_dtype dt,
+                                  void *cbuf, float *ybuf, void *out, int32_t *err, hipStream_t stream) {
+  const int d = p->d, h = p->h;
+  if (dt == SM_BF16) {
+    if (launch_pool<uint16_t>((const uint16_t *)G1, gidx, g_rows, span_offsets, num_spans, total_rows,
+                              (const uint16_t *)p->Q, (const uint16_t *)p->g_kv, (const uint16_t *)p->beta_kv,
+                              p->ln_eps, d, h, (uint16_t *)cbuf, err, stream) != hipSuccess)
       return SM_EHIP;
     if (num_spans <= kSkinnyMaxM)
       launch_skinny<float>((const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
@@ -1027,13 +1053,9 @@ SM_API sm_status sm_merge_spans(const void *emb, int64_t emb_rows, const int32_t
     hipLaunchKernelGGL(ln_rows_kernel<uint16_t>, dim3(num_spans), dim3(kPoolThreads), 0, stream, ybuf,
                        (const uint16_t *)p->g_o, (const uint16_t *)p->beta_o, p->ln_eps, d, (uint16_t *)out);
   } else {
-    hipLaunchKernelGGL(gemm_f32_nt_gelu, dim3(d / kFT, (total_rows + kFT - 1) / kFT), dim3(256), 0, stream,
-                       (const float *)emb, row_idx, emb_rows, (const float *)p->W_kv, (const float *)p->b_kv,
-                       (float *)g1, total_rows, d, d, err);
-    if (hipGetLastError() != hipSuccess) return SM_EHIP;
-    if (launch_pool<float>((const float *)g1, span_offsets, num_spans, total_rows, (const float *)p->Q,
-                           (const float *)p->g_kv, (const float *)p->beta_kv, p->ln_eps, d, h, (float *)cbuf, err,
-                           stream) != hipSuccess)
+    if (launch_pool<float>((const float *)G1, gidx, g_rows, span_offsets, num_spans, total_rows,
+                           (const float *)p->Q, (const float *)p->g_kv, (const float *)p->beta_kv, p->ln_eps, d, h,
+                           (float *)cbuf, err, stream) != hipSuccess)
       return SM_EHIP;
     hipLaunchKernelGGL(gemm_f32_nt_gelu, dim3(d / kFT, (num_spans + kFT - 1) / kFT), dim3(256), 0, stream,
                        (const float *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans, (const float *)p->W_o,
@@ -1043,6 +1065,62 @@ SM_API sm_status sm_merge_spans(const void *emb, int64_t emb_rows, const int32_t
                        (const float *)p->g_o, (const float *)p->beta_o, p->ln_eps, d, (float *)out);
   }
   return hipGetLastError() == hipSuccess ? SM_OK : SM_EHIP;
+}
+
+SM_API sm_status sm_merge_spans(const void *emb, int64_t emb_rows, const int32_t *row_idx, int total_rows,
+                                const int32_t *span_offsets, int num_spans, const sm_merge_params *p,
+                                sm_dtype dt, void *out, void *ws, size_t ws_bytes, int32_t *err,
+                                hipStream_t stream) {
+  if (total_rows < 0 || num_spans < 0) return SM_EINVAL;
+  const sm_status pst = merge_param_check(p, dt);
+  if (pst != SM_OK) return pst;
+  const int d = p->d;
+  if (num_spans == 0) return total_rows == 0 ? SM_OK : SM_EINVAL;
+  if (total_rows < num_spans) return SM_EINVAL;
+  if (!emb || emb_rows <= 0 || !row_idx || !span_offsets || !out || !ws || !err) return SM_EINVAL;
+  if (ws_bytes < sm_merge_workspace_bytes(total_rows, num_spans, d, dt)) return SM_EINVAL;
+  if ((total_rows + kBM - 1) / kBM > 65535 || (num_spans + kBM - 1) / kBM > 65535) return SM_EINVAL;
+
+  const size_t es = dt == SM_BF16 ? 2 : 4;
+  char *wsb = (char *)ws;
+  void *g1 = wsb;
+  void *cbuf = wsb + align256((size_t)total_rows * d * es);
+  float *ybuf = (float *)(wsb + align256((size_t)total_rows * d * es) + align256((size_t)num_spans * d * es));
+  const sm_status st = first_stage(emb, row_idx, emb_rows, total_rows, p, dt, g1, err, stream);
+  if (st != SM_OK) return st;
+  return pool_and_project(g1, nullptr, total_rows, total_rows, span_offsets, num_spans, p, dt, cbuf, ybuf, out, err,
+                          stream);
+}
+
+SM_API sm_status sm_merge_token_table(const void *emb, int64_t emb_rows, const sm_merge_params *p, sm_dtype dt,
+                                      void *table, int32_t *err, hipStream_t stream) {
+  const sm_status pst = merge_param_check(p, dt);
+  if (pst != SM_OK) return pst;
+  if (emb_rows <= 0 || emb_rows > INT32_MAX || !emb || !table || !err) return SM_EINVAL;
+  if ((emb_rows + kBM - 1) / kBM > 65535) return SM_EINVAL;
+  return first_stage(emb, nullptr, emb_rows, (int)emb_rows, p, dt, table, err, stream);
+}
+
+SM_API sm_status sm_merge_spans_tabled(const void *table, int64_t table_rows, const int32_t *row_idx,
+                                       int total_rows, const int32_t *span_offsets, int num_spans,
+                                       const sm_merge_params *p, sm_dtype dt, void *out, void *ws, size_t ws_bytes,
+                                       int32_t *err, hipStream_t stream) {
+  if (total_rows < 0 || num_spans < 0) return SM_EINVAL;
+  const sm_status pst = merge_param_check(p, dt);
+  if (pst != SM_OK) return pst;
+  const int d = p->d;
+  if (num_spans == 0) return total_rows == 0 ? SM_OK : SM_EINVAL;
+  if (total_rows < num_spans) return SM_EINVAL;
+  if (!table || table_rows <= 0 || !row_idx || !span_offsets || !out || !ws || !err) return SM_EINVAL;
+  if (ws_bytes < sm_merge_workspace_bytes(0, num_spans, d, dt)) return SM_EINVAL;
+  if ((num_spans + kBM - 1) / kBM > 65535) return SM_EINVAL;
+
+  const size_t es = dt == SM_BF16 ? 2 : 4;
+  char *wsb = (char *)ws;
+  void *cbuf = wsb;
+  float *ybuf = (float *)(wsb + align256((size_t)num_spans * d * es));
+  return pool_and_project(table, row_idx, table_rows, total_rows, span_offsets, num_spans, p, dt, cbuf, ybuf, out,
+                          err, stream);
 }
 
 SM_API const char *sm_status_string(sm_status s) {

@@ -24,6 +24,7 @@ MAX_REQUESTS = 1024
 _P, _I, _L, _F, _Z = C.c_void_p, C.c_int, C.c_int64, C.c_float, C.c_size_t
 
 EXPORTED = ("sm_status_string", "sm_merge_workspace_bytes", "sm_merge_spans",
+            "sm_merge_token_table", "sm_merge_spans_tabled",
             "sm_pack_spans", "sm_kv_rollback", "sm_kv_append",
             "sm_decode_workspace_bytes", "sm_decode_attention", "sm_decode_step",
             "sm_prefill_attention", "sm_rules_build_workspace_bytes", "sm_rules_build",
@@ -77,6 +78,11 @@ def load(path: str = LIB_PATH):
     L.sm_merge_spans.argtypes = [_P, _L, _P, _I, _P, _I, C.POINTER(MergeParams), _I,
                                  _P, _P, _Z, _P, _P]
     L.sm_merge_spans.restype = _I
+    L.sm_merge_token_table.argtypes = [_P, _L, C.POINTER(MergeParams), _I, _P, _P, _P]
+    L.sm_merge_token_table.restype = _I
+    L.sm_merge_spans_tabled.argtypes = [_P, _L, _P, _I, _P, _I, C.POINTER(MergeParams), _I,
+                                        _P, _P, _Z, _P, _P]
+    L.sm_merge_spans_tabled.restype = _I
     L.sm_pack_spans.argtypes = [_I, _P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _L,
                                 _P, _I, _I, _P, _P, _P]
     L.sm_pack_spans.restype = _I
@@ -171,6 +177,33 @@ def merge_spans(emb, row_idx, span_offsets, params: dict, h: int, out, ws, err,
                                _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
                                _ptr(err), _stream(stream))
     _check(st, "sm_merge_spans")
+
+
+def _merge_params(d: int, h: int, params: dict, ln_eps: float):
+    return MergeParams(d, h, ln_eps, *(_ptr(params[k]) for k in
+                       ("Q", "W_kv", "b_kv", "g_kv", "beta_kv", "W_o", "b_o", "g_o", "beta_o")))
+
+
+def merge_token_table(emb, params: dict, h: int, table, err, ln_eps: float = 1e-5, stream=None):
+    """table[v] = GELU(Linear_kv(emb[v])) for every row of ``emb``."""
+    p = _merge_params(emb.shape[1], h, params, ln_eps)
+    st = load().sm_merge_token_table(_ptr(emb), emb.shape[0], C.byref(p), dtype_code(emb.dtype),
+                                     _ptr(table), _ptr(err), _stream(stream))
+    _check(st, "sm_merge_token_table")
+
+
+def merge_spans_tabled(table, row_idx, span_offsets, params: dict, h: int, out, ws, err,
+                       ln_eps: float = 1e-5, total_rows: Optional[int] = None, stream=None):
+    """The surrogates of merge_spans, the first stage read from ``table``
+    (rows = token ids)."""
+    S = span_offsets.numel() - 1
+    R = row_idx.numel() if total_rows is None else total_rows
+    p = _merge_params(table.shape[1], h, params, ln_eps)
+    st = load().sm_merge_spans_tabled(_ptr(table), table.shape[0], _ptr(row_idx), R,
+                                      _ptr(span_offsets), S, C.byref(p), dtype_code(table.dtype),
+                                      _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
+                                      _ptr(err), _stream(stream))
+    _check(st, "sm_merge_spans_tabled")
 
 
 # --------------------------------------------------------------------------
