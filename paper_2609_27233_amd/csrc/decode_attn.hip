@@ -647,7 +647,7 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
   bool may_write = false; // this workgroup stores the new row (if the append commits)
   bool late = false;      // new length = max_len + 1 exactly: ERANGE iff the append commits
   bool own_can = false;
-  float kq[4] = {0.f, 0.f, 0.f, 0.f}, vrow = 0.f;
+  uint32_t kn2 = 0u, qn2[4] = {0u, 0u, 0u, 0u};  // the new token's score inputs (bf16 pairs)
   uint16_t krow_e = 0, vrow_e = 0;
   int32_t *esink = a.err;
 
@@ -657,24 +657,16 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
       return;
     }
     esink = nullptr;  // errors travel with the arrival
-    // wave 3 (no page ids to fetch at these sizes) works out the whole
-    // append: two round trips and register work, beside the other waves'
-    // chain of this request's id, length and page ids
+    // wave 3 (no page ids to fetch at these sizes) issues the reads the
+    // append's plan needs, two round trips beside the other waves' chain of
+    // this request's id, length and page ids; the plan itself is worked
+    // out after the streaming loop, where it is first needed
     if (w == kDecWaves - 1) step_plan_read1(a, pr);
     s = a.seq_ids[i];
     const int frozen = *a.err != 0;
     const bool own_ok = s >= 0 && s < a.max_seqs;
     if (w == kDecWaves - 1) step_plan_read2(a, pr);
     L_pool = own_ok ? a.lengths[s] : 0;
-    if (w == kDecWaves - 1) {  // the plan, as soon as its reads are in
-      PlanOut po;
-      plan_any(a, pr, po);
-      const int pop_i = request_value(po.pop, i);
-      if (lane == 0) {
-        step_plan_sh[0] = po.ok;
-        step_plan_sh[1] = pop_i;
-      }
-    }
     if (!own_ok || L_pool < 0 || L_pool > (a.max_blocks << bs_log2)) st = SM_ERR_EINVAL;
     own_can = !frozen && st == 0 && (int64_t)L_pool + 1 <= a.cap;
     if (st == 0) {  // chunked for the appended length whenever this request can append
@@ -711,25 +703,19 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     // l, l + 64 of query heads w, w + 4, ...
     const uint16_t *kn = (const uint16_t *)a.k_new + ((int64_t)i * a.Hkv + g) * DH;
     const uint16_t *vn = (const uint16_t *)a.v_new + ((int64_t)i * a.Hkv + g) * DH;
-    if (has_new && 2 * lane < DH) {  // all loads first (one round trip), then the products
+    if (has_new && 2 * lane < DH) {  // loaded now, multiplied after the streaming loop
       const uint16_t *qg = (const uint16_t *)a.q + ((int64_t)i * a.Hq + g * a.G) * DH + 2 * lane;
-      const uint32_t kk2 = *(const uint32_t *)(kn + 2 * lane);
-      uint32_t qq2[4];
+      kn2 = *(const uint32_t *)(kn + 2 * lane);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int hh = w + kDecWaves * u;
-        qq2[u] = hh < a.G ? *(const uint32_t *)(qg + hh * DH) : 0u;
+        qn2[u] = hh < a.G ? *(const uint32_t *)(qg + hh * DH) : 0u;
       }
-      const float k0 = __uint_as_float(kk2 << 16), k1 = __uint_as_float(kk2 & 0xffff0000u);
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        kq[u] = __uint_as_float(qq2[u] << 16) * k0 + __uint_as_float(qq2[u] & 0xffff0000u) * k1;
     }
     may_write = own_can && (has_new || (c == 0 && (st == SM_ERR_ERANGE || late)));
     if (may_write && tid < DH) {
       krow_e = kn[tid];
       vrow_e = vn[tid];
-      vrow = bf16_to_f32(vrow_e);
     }
     {
       const bool wave_bad = __ballot(bad_page) != 0;
@@ -757,11 +743,12 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     }
   }
 
-  // Fused step, once the plan is published: this workgroup's share of the
-  // append.  Decided right away; the new row's stores and the arrival are
-  // issued only after the workgroup's last tile loads (stores and atomics
-  // count in the same wait counter as loads, so issued earlier they would
-  // hold up the first tile waits).
+  // Fused step, after the streaming loop (or right away for a workgroup
+  // that streams nothing): wave 3 works out the plan from the reads it
+  // issued in the prologue and publishes it, then every wave decides this
+  // workgroup's share of the append.  The new row's stores and the arrival
+  // follow (stores and atomics count in the same wait counter as loads, so
+  // issued before the tile loads they would hold up the first tile waits).
   bool step_ok = false, late_range = false;
   int step_errs = 0, new_blk = -1;
   auto step_decide = [&]() __attribute__((always_inline)) {
@@ -785,35 +772,51 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
       }
     }
   };
+  auto step_plan_decide = [&]() __attribute__((always_inline)) {
+    if (w == kDecWaves - 1) {
+      PlanOut po;
+      plan_any(a, pr, po);
+      const int pop_i = request_value(po.pop, i);
+      if (lane == 0) {
+        step_plan_sh[0] = po.ok;
+        step_plan_sh[1] = pop_i;
+      }
+    }
+    lds_barrier();
+    step_decide();
+  };
   auto step_finish = [&]() __attribute__((always_inline)) {
     if (new_blk >= 0 && tid < DH) {  // the appended row of head g into its page
       const int64_t page_elems = (int64_t)bs * DH;
       const int slot = L_pool & (bs - 1);
       uint16_t *kd = (uint16_t *)a.k_pool + ((int64_t)new_blk * a.Hkv + g) * page_elems + (int64_t)slot * DH;
       uint16_t *vd = (uint16_t *)a.v_pool + ((int64_t)new_blk * a.Hkv + g) * page_elems + slot;
-      kd[tid] = krow_e;
-      vd[(int64_t)tid * bs] = vrow_e;
+      // streaming stores: the scattered 2-byte V row is not left dirty in L2
+      // for the end-of-kernel writeback
+      __builtin_nontemporal_store(krow_e, kd + tid);
+      __builtin_nontemporal_store(vrow_e, vd + (int64_t)tid * bs);
     }
     if (tid == 0) step_arrive_nowait(a, step_errs);
     if (has_new) {
+      const float k0 = __uint_as_float(kn2 << 16), k1 = __uint_as_float(kn2 & 0xffff0000u);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int hh = w + kDecWaves * u;
-        const float d = wave_sum(kq[u]);
+        const float kq = __uint_as_float(qn2[u] << 16) * k0 + __uint_as_float(qn2[u] & 0xffff0000u) * k1;
+        const float d = wave_sum(kq);
         if (hh < a.G && lane == 0) step_sn[hh] = d * a.scale_log2e;
       }
-      if (tid < DH) step_vn[tid] = vrow;
+      if (tid < DH) step_vn[tid] = bf16_to_f32(vrow_e);
     }
   };
 
-  if constexpr (STEP) {
-    step_decide();
-    if (late_range) st = SM_ERR_ERANGE;  // zero rows; the bit travels with the arrival
-  }
-
   auto body = [&]() {
     if constexpr (STEP) {
-      if (!(st == 0 && L > 0 && work && pages_ok)) step_finish();
+      if (!(st == 0 && L > 0 && work && pages_ok)) {
+        step_plan_decide();
+        if (late_range) st = SM_ERR_ERANGE;  // zero rows; the bit travels with the arrival
+        step_finish();
+      }
     }
     if (st != 0 || L == 0) {
       if (c == 0) write_zero_rows<uint16_t>(a, i, g, DH, st, esink);
@@ -941,7 +944,13 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
       if (tile + 2 * step < ntiles) load(bufA, tile + 2 * step);
       compute(bufB, tile + step);
     }
-    if constexpr (STEP) step_finish();
+    if constexpr (STEP) {
+      // a request whose appended length reaches max_len + 1 streamed its
+      // old length; once the append is known to commit it gets zero rows
+      // and ERANGE, carried as an unusable partial into the combine
+      step_plan_decide();
+      step_finish();
+    }
 
     // per-head totals of this wave (lanes r, r+16, r+32, r+48 share head r)
     float l_tot;
@@ -985,6 +994,12 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
           acc = acc * f + step_vn[dd] * fN;
           ls = ls * f + fN;
           M = M2;
+        }
+      }
+      if constexpr (STEP) {
+        if (late_range) {
+          M = 0.f;
+          ls = -1.f;  // marks the chunk as unusable: the group's rows become zero
         }
       }
       if (nc == 1) {  // the only chunk: write the result directly
