@@ -14,7 +14,10 @@ compacted paged cache (16-token pages) are one fused launch
 One benchmark step runs that whole job for R resident batches ("replicas")
 of 16 sequences, served round-robin the way a server alternates between
 batches; R * (bytes per attention launch) is several times the 256 MB
-Infinity Cache, so no attention launch finds its KV in the MALL.
+Infinity Cache, so no attention launch finds its KV in the MALL.  The
+merge module's first stage comes from the token table (built once, at set
+up); the batches reach their merge steps together, so their fresh spans go
+to the merge module together, 64 spans per call.
 
 Printed: one JSON line with the whole-job decode throughput, the fused
 append + decode attention kernel's achieved HBM bandwidth against the 8 TB/s
@@ -116,14 +119,22 @@ class Job:
         # a synthetic generated-token stream
         self.merge_steps = [s for s in range(steps) if w.merge_every and s % w.merge_every == w.merge_every - 1]
         rng = np.random.RandomState(w.seed + 5)
+        # the resident batches reach a merge step together: their fresh spans
+        # go to the merge module together, 64 spans (4 batches of 16) per call
+        # (the skinny GEMM's row limit), each batch then rolls back its own
+        # cache
+        self.merge_group = max(1, 64 // B)
+        G = self.merge_group
         self.dmerge = {}
         for s in self.merge_steps:
             n = wl.decode_merge_lengths(w, s)
             offs = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
-            self.dmerge[s] = dict(n=n, k=i32(n - 1), offs=i32(offs), rows=int(offs[-1]),
-                                  row_idx=i32(rng.randint(0, w.vocab, size=int(offs[-1]))))
-        self.zdec = torch.empty((B, w.d), dtype=bf, device=dev)
-        self.dmerge_ws = torch.empty(sm.merge_workspace_bytes(B * max(w.merge_n), B, w.d, bf),
+            rows = int(offs[-1])
+            row_idx = rng.randint(0, w.vocab, size=rows)
+            goffs = np.concatenate([offs[:-1] + j * rows for j in range(G)] + [[G * rows]]).astype(np.int32)
+            self.dmerge[s] = dict(n=n, k=i32(n - 1), rows=rows, g_offs=i32(goffs), g_row_idx=i32(np.tile(row_idx, G)))
+        self.zdec = torch.empty((G * B, w.d), dtype=bf, device=dev)
+        self.dmerge_ws = torch.empty(sm.merge_workspace_bytes(G * B * max(w.merge_n), G * B, w.d, bf),
                                      dtype=torch.uint8, device=dev)
         # host-side copy of the length schedule (for the algorithmic bytes)
         self.len_sched = []
@@ -190,16 +201,20 @@ class Job:
         return L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], row_idx, rows, offs, S,
                                 C.byref(self.mp), bf, z, ws.data_ptr(), ws.numel(), self.err.data_ptr(), st)
 
-    def _merge(self, r, s, st):
-        """Decode-time merge of batch r before decode step s: the merge
-        module on each sequence's freshly completed span and the roll back of
-        its n-1 entries (the surrogate's K/V is then the step's appended row)."""
+    def _merge(self, rs, s, st):
+        """Decode-time merge of batches rs (at most merge_group of them)
+        before decode step s: the merge module on every sequence's freshly
+        completed span, in one call, and each batch's roll back of n-1
+        entries per sequence (the surrogate's K/V is then the step's
+        appended row)."""
         L, w = self.L, self.w
-        B, bf = w.batch, self.sm.SM_BF16
+        B = w.batch
         m = self.dmerge[s]
-        rc = self._merge_call(m["row_idx"].data_ptr(), m["rows"], m["offs"].data_ptr(), B, self.zdec.data_ptr(),
-                              self.dmerge_ws, st)
-        rc |= L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), m["k"].data_ptr(), B, st)
+        S = len(rs) * B
+        rc = self._merge_call(m["g_row_idx"].data_ptr(), len(rs) * m["rows"], m["g_offs"].data_ptr(), S,
+                              self.zdec.data_ptr(), self.dmerge_ws, st)
+        for r in rs:
+            rc |= L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), m["k"].data_ptr(), B, st)
         if rc:
             raise RuntimeError(f"decode-time merge launch failed at step {s}: {rc}")
 
@@ -253,12 +268,15 @@ class Job:
                 self.upd_done[r].record(upd_stream)
         for s in range(w.decode_steps):
             if s in self.dmerge:
-                for r in range(R):
+                for g0 in range(0, R, self.merge_group):
+                    rs = range(g0, min(R, g0 + self.merge_group))
                     if overlap:
-                        upd_stream.wait_event(self.attn_done[r])
-                    self._merge(r, s, sb)
+                        for r in rs:
+                            upd_stream.wait_event(self.attn_done[r])
+                    self._merge(rs, s, sb)
                     if overlap:
-                        self.upd_done[r].record(upd_stream)
+                        for r in rs:
+                            self.upd_done[r].record(upd_stream)
             if events is not None:
                 events[0][s].record(stream)
             for r in range(R):
