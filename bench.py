@@ -15,15 +15,18 @@ One benchmark step runs that whole job for R resident batches ("replicas")
 of 16 sequences, served round-robin the way a server alternates between
 batches; R * (bytes per attention launch) is several times the 256 MB
 Infinity Cache, so no attention launch finds its KV in the MALL.  The
-merge module's first stage comes from the token table (built once, at set
-up); the batches reach their merge steps together, so their fresh spans go
-to the merge module together, 64 spans per call.
+batches' decode steps are spread over four streams ("lanes": batch r on
+stream r % 4, each with its own workspaces), so that one launch's drain and
+combine overlap other launches' streaming.  The merge module's first
+stage comes from the token table (built once, at set up); a stream's
+batches reach their merge steps together, so their fresh spans go to the
+merge module together, 64 spans per call.
 
 Printed: one JSON line with the whole-job decode throughput, the fused
 append + decode attention kernel's achieved HBM bandwidth against the 8 TB/s
-roofline (measured live with HIP events on the launch stream around each
-decode step's back-to-back launches), and the CPU oracle timed on a bounded
-sample of the same job.
+roofline (its launch duration measured live with HIP events around each
+decode step's back-to-back launches in a one-stream pass of the same job;
+`roofline.overlapped` gives the rate of the lanes' overlapped launches), and the CPU oracle timed on a bounded sample of the same job.
 """
 from __future__ import annotations
 
@@ -58,7 +61,7 @@ def log(*a):
 class Job:
     """Device state of R resident batches of one workload."""
 
-    def __init__(self, w, R, dev, seed_base=0, token_table=True):
+    def __init__(self, w, R, dev, seed_base=0, token_table=True, lanes=1):
         import torch
         from paper_2609_27233_amd import lib as sm
         from paper_2609_27233_amd import workload as wl
@@ -110,8 +113,13 @@ class Job:
         self.Kt = [wl.randn((B, H, D), bf, g, device=dev) for _ in range(self.nin)]
         self.Vt = [wl.randn((B, H, D), bf, g, device=dev) for _ in range(self.nin)]
         self.q = [wl.randn((B, Hq, D), bf, g, device=dev) for _ in range(self.nin)]
-        self.out = torch.empty((B, Hq, D), dtype=bf, device=dev)
-        self.dec_ws = torch.zeros(sm.decode_workspace_bytes(B, Hq, D, self.max_len), dtype=torch.uint8, device=dev)
+        # batch r's decode steps run on lane (stream) r % lanes; each lane has
+        # its own output, decode workspace and decode-time merge buffers, so
+        # that the lanes' launches can overlap
+        self.lanes = NL = max(1, min(lanes, R))
+        self.out = [torch.empty((B, Hq, D), dtype=bf, device=dev) for _ in range(NL)]
+        self.dec_ws = [torch.zeros(sm.decode_workspace_bytes(B, Hq, D, self.max_len), dtype=torch.uint8, device=dev)
+                       for _ in range(NL)]
         self.ids = i32(np.arange(B))
         self.one_row = i32(np.arange(B + 1))
         self.kreset = torch.empty(B, dtype=torch.int32, device=dev)
@@ -119,12 +127,16 @@ class Job:
         # a synthetic generated-token stream
         self.merge_steps = [s for s in range(steps) if w.merge_every and s % w.merge_every == w.merge_every - 1]
         rng = np.random.RandomState(w.seed + 5)
-        # the resident batches reach a merge step together: their fresh spans
-        # go to the merge module together, 64 spans (4 batches of 16) per call
-        # (the skinny GEMM's row limit), each batch then rolls back its own
-        # cache
+        # the resident batches reach a merge step together: the fresh spans
+        # of a lane's batches go to the merge module together, 64 spans (4
+        # batches of 16) per call (the skinny GEMM's row limit), each batch
+        # then rolls back its own cache
         self.merge_group = max(1, 64 // B)
         G = self.merge_group
+        self.merge_groups = []
+        for lane in range(NL):
+            rs = list(range(lane, R, NL))
+            self.merge_groups.append([rs[i:i + G] for i in range(0, len(rs), G)])
         self.dmerge = {}
         for s in self.merge_steps:
             n = wl.decode_merge_lengths(w, s)
@@ -133,9 +145,9 @@ class Job:
             row_idx = rng.randint(0, w.vocab, size=rows)
             goffs = np.concatenate([offs[:-1] + j * rows for j in range(G)] + [[G * rows]]).astype(np.int32)
             self.dmerge[s] = dict(n=n, k=i32(n - 1), rows=rows, g_offs=i32(goffs), g_row_idx=i32(np.tile(row_idx, G)))
-        self.zdec = torch.empty((G * B, w.d), dtype=bf, device=dev)
-        self.dmerge_ws = torch.empty(sm.merge_workspace_bytes(G * B * max(w.merge_n), G * B, w.d, bf),
-                                     dtype=torch.uint8, device=dev)
+        self.zdec = [torch.empty((G * B, w.d), dtype=bf, device=dev) for _ in range(NL)]
+        self.dmerge_ws = [torch.empty(sm.merge_workspace_bytes(G * B * max(w.merge_n), G * B, w.d, bf),
+                                      dtype=torch.uint8, device=dev) for _ in range(NL)]
         # host-side copy of the length schedule (for the algorithmic bytes)
         self.len_sched = []
         lens = np.full(B, self.L0, np.int64)
@@ -145,8 +157,6 @@ class Job:
             else:
                 lens = lens + 1
             self.len_sched.append(lens.copy())
-        self.attn_done = [torch.cuda.Event() for _ in range(R)]
-        self.upd_done = [torch.cuda.Event() for _ in range(R)]
         torch.cuda.synchronize()
         self._prep_ctypes()
         # the merge module's first stage for every vocabulary row, built once
@@ -201,18 +211,18 @@ class Job:
         return L.sm_merge_spans(self.emb.data_ptr(), self.emb.shape[0], row_idx, rows, offs, S,
                                 C.byref(self.mp), bf, z, ws.data_ptr(), ws.numel(), self.err.data_ptr(), st)
 
-    def _merge(self, rs, s, st):
-        """Decode-time merge of batches rs (at most merge_group of them)
-        before decode step s: the merge module on every sequence's freshly
-        completed span, in one call, and each batch's roll back of n-1
-        entries per sequence (the surrogate's K/V is then the step's
-        appended row)."""
+    def _merge(self, rs, s, lane, st):
+        """Decode-time merge of batches rs (at most merge_group of them, all
+        on `lane`) before decode step s: the merge module on every
+        sequence's freshly completed span, in one call, and each batch's roll
+        back of n-1 entries per sequence (the surrogate's K/V is then the
+        step's appended row)."""
         L, w = self.L, self.w
         B = w.batch
         m = self.dmerge[s]
         S = len(rs) * B
         rc = self._merge_call(m["g_row_idx"].data_ptr(), len(rs) * m["rows"], m["g_offs"].data_ptr(), S,
-                              self.zdec.data_ptr(), self.dmerge_ws, st)
+                              self.zdec[lane].data_ptr(), self.dmerge_ws[lane], st)
         for r in rs:
             rc |= L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), m["k"].data_ptr(), B, st)
         if rc:
@@ -223,33 +233,42 @@ class Job:
         surrogate) and attend, in one launch."""
         L, w = self.L, self.w
         j = s % self.nin
+        lane = r % self.lanes
+        ws = self.dec_ws[lane]
         rc = L.sm_decode_step(self.descs[r], self.ids.data_ptr(), w.batch, self.Kt[j].data_ptr(),
                               self.Vt[j].data_ptr(), self.q[j].data_ptr(), w.num_q_heads, w.head_dim ** -0.5,
-                              self.max_len, self.out.data_ptr(), self.dec_ws.data_ptr(), self.dec_ws.numel(), st)
+                              self.max_len, self.out[lane].data_ptr(), ws.data_ptr(), ws.numel(), st)
         if rc:
             raise RuntimeError(f"decode step launch failed at step {s}: {rc}")
 
-    def run(self, stream, upd_stream, events=None):
+    def run(self, streams, events=None):
         """One benchmark step: the whole job for every resident batch.
 
-        Fused decode steps run on `stream`; prompt compression and
-        decode-time merges run on `upd_stream`, each waiting only for its own
-        batch's previous step.  When both are the same stream everything runs
-        in order (the default); with two streams batch r's merge overlaps
-        the decode steps of the other batches."""
+        Lane l's batches (r % lanes == l) run their decode steps, and their
+        decode-time merges, in order on streams[l % len(streams)]; the lanes
+        share nothing, so their launches overlap: one lane's workgroups
+        stream their KV while the other's launch drains its last tiles and
+        combines.  Prompt compression runs on streams[0] (its buffers are
+        shared) after every lane's previous job, and the other lanes wait
+        for it.  With `events` (one stream only) each step's launches are
+        bracketed by events[0][s] and events[1][s]."""
         import torch
         L, w = self.L, self.w
-        B, bf = w.batch, self.sm.SM_BF16
-        sa, sb = stream.cuda_stream, upd_stream.cuda_stream
-        overlap = sa != sb
+        B = w.batch
         R = self.R
+        if events is not None and len(streams) != 1:
+            raise ValueError("per-step events need a single stream")
+        s0 = streams[0]
+        sb = s0.cuda_stream
+        lane_st = [streams[l % len(streams)] for l in range(self.lanes)]
+        for st in streams[1:]:
+            s0.wait_stream(st)
         # prompt compression of every batch (after its previous job's last
         # decode step)
         for r in range(R):
-            c, dp = self.caches[r], self.dev_prompts[r]
-            if overlap:
-                upd_stream.wait_event(self.attn_done[r])
-            with torch.cuda.stream(upd_stream):
+            dp = self.dev_prompts[r]
+            c = self.caches[r]
+            with torch.cuda.stream(s0):
                 self.kreset.copy_(c.lengths[:B])   # evict the previous job's sequences
             rc = L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), self.kreset.data_ptr(), B, sb)
             rc |= self._merge_call(dp["row_idx"].data_ptr(), dp["rows"], dp["span_offsets"].data_ptr(), dp["S"],
@@ -258,40 +277,68 @@ class Job:
                                   dp["span_start"].data_ptr(), dp["span_len"].data_ptr(),
                                   dp["seq_span_offsets"].data_ptr(), self.pi.data_ptr(), self.po.data_ptr(),
                                   self.ps.data_ptr(), dp["token_ids"].data_ptr(), self.emb.data_ptr(),
-                                  self.emb.shape[0], self.z.data_ptr(), w.d, bf, self.packed.data_ptr(),
+                                  self.emb.shape[0], self.z.data_ptr(), w.d, self.sm.SM_BF16, self.packed.data_ptr(),
                                   self.err.data_ptr(), sb)
             rc |= L.sm_kv_append(self.descs[r], self.ids.data_ptr(), self.po.data_ptr(), B, self.packed_rows[r],
                                  self.Kp.data_ptr(), self.Vp.data_ptr(), sb)
             if rc:
                 raise RuntimeError(f"prompt compression launch failed: {rc}")
-            if overlap:
-                self.upd_done[r].record(upd_stream)
+        for st in streams[1:]:
+            st.wait_stream(s0)
         for s in range(w.decode_steps):
             if s in self.dmerge:
-                for g0 in range(0, R, self.merge_group):
-                    rs = range(g0, min(R, g0 + self.merge_group))
-                    if overlap:
-                        for r in rs:
-                            upd_stream.wait_event(self.attn_done[r])
-                    self._merge(rs, s, sb)
-                    if overlap:
-                        for r in rs:
-                            self.upd_done[r].record(upd_stream)
+                for lane, groups in enumerate(self.merge_groups):
+                    for rs in groups:
+                        self._merge(rs, s, lane, lane_st[lane].cuda_stream)
             if events is not None:
-                events[0][s].record(stream)
+                events[0][s].record(s0)
             for r in range(R):
-                if overlap:
-                    stream.wait_event(self.upd_done[r])
-                self._step(r, s, sa)
-                if overlap:
-                    self.attn_done[r].record(stream)
+                self._step(r, s, lane_st[r % self.lanes].cuda_stream)
             if events is not None:
-                events[1][s].record(stream)
+                events[1][s].record(s0)
 
     def check_errors(self):
         bits = [c.error_bits() for c in self.caches] + [int(self.err.item())]
         if any(bits):
             raise RuntimeError(f"device error bits set: {bits}")
+
+
+def lanes_report(job, streams, rounds):
+    """Fused decode steps of every resident batch back to back over the
+    job's caches as the job left them, on one stream and then on the job's
+    lanes: the rate at which the overlapped launches move the kernel's
+    algorithmic bytes.  Each round appends one row per sequence."""
+    import torch
+    w, B = job.w, job.w.batch
+    res = {}
+    for name, sts in (("one_stream", streams[:1]), ("lanes", streams)):
+        lane_st = [sts[l % len(sts)] for l in range(job.lanes)]
+        for timed in (False, True):
+            lens0 = np.stack([c.lengths[:B].cpu().numpy().astype(np.int64) for c in job.caches])
+            n = rounds if timed else 1
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(sts[0])
+            for st in sts[1:]:
+                st.wait_event(e0)
+            for it in range(n):
+                for r in range(job.R):
+                    job._step(r, it, lane_st[r % job.lanes].cuda_stream)
+            for st in sts[1:]:
+                sts[0].wait_stream(st)
+            e1.record(sts[0])
+            torch.cuda.synchronize()
+        nbytes = sum(job.decode_bytes(lens0[r] + it + 1) for it in range(n) for r in range(job.R))
+        us = e0.elapsed_time(e1) * 1e3 / (n * job.R)
+        res[name] = {"us_per_launch": round(us, 3), "achieved": round(nbytes / (us * 1e-6 * n * job.R) / 1e9, 1)}
+    job.check_errors()
+    ach = res["lanes"]["achieved"]
+    return {"lanes": job.lanes, "us_per_launch": res["lanes"]["us_per_launch"], "achieved": ach,
+            "frac": round(ach / PEAK_HBM_GBS, 4), "one_stream_us_per_launch": res["one_stream"]["us_per_launch"],
+            "mean_cache_len": round(float(np.mean([c.lengths[:B].cpu().numpy() for c in job.caches])), 1),
+            "note": "the fused step of every resident batch, %d rounds back to back over the job's caches, batch r "
+                    "on stream r %% %d: bytes of all launches over the time from the first start to the last end; "
+                    "overlapping launches have no duration of their own" % (rounds, job.lanes)}
 
 
 def _time(fn, stream, reps):
@@ -329,7 +376,7 @@ def extras_report(job, stream, attn_us):
     def attn_job():
         for d0 in descs0:
             L.sm_decode_attention(d0, ids.data_ptr(), B, job.q[0].data_ptr(), Hq, D ** -0.5, job.max_len,
-                                  job.out.data_ptr(), ws0.data_ptr(), ws0.numel(), st)
+                                  job.out[0].data_ptr(), ws0.data_ptr(), ws0.numel(), st)
     ms0 = _time(attn_job, stream, 16) / job.R
     lens_end = job.caches[0].lengths[:B].cpu().numpy().astype(np.int64)
     b0 = job.decode_bytes(lens_end, fused=False)
@@ -361,7 +408,7 @@ def extras_report(job, stream, attn_us):
     def attn_all():
         for d in descs:
             L.sm_decode_attention(d, ids.data_ptr(), B, job.q[0].data_ptr(), Hq, D ** -0.5, Lu,
-                                  job.out.data_ptr(), ws.data_ptr(), ws.numel(), st)
+                                  job.out[0].data_ptr(), ws.data_ptr(), ws.numel(), st)
     ms = _time(attn_all, stream, 16) / job.R
     ubytes = job.decode_bytes(np.full(B, Lu), fused=False)
     out["uncompressed_control"] = {
@@ -858,8 +905,8 @@ def main():
                     help="only time the prefill attention over the compacted and uncompressed prompt batch")
     ap.add_argument("--no-token-table", action="store_true",
                     help="run the job's merges from the embeddings (sm_merge_spans) instead of the token table")
-    ap.add_argument("--overlap", action="store_true",
-                    help="run cache updates on a second stream, overlapped with other batches' attention")
+    ap.add_argument("--lanes", type=int, default=4,
+                    help="streams the resident batches' decode steps are spread over (batch r on stream r %% lanes)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build measures the single-GPU hot path "
@@ -903,37 +950,45 @@ def main():
     w = wl.WORKLOADS[2]
     if args.decode_steps is not None:
         w = dataclasses.replace(w, decode_steps=args.decode_steps)
-    job = Job(w, args.replicas, dev, token_table=not args.no_token_table)
+    job = Job(w, args.replicas, dev, token_table=not args.no_token_table, lanes=args.lanes)
     stream = torch.cuda.current_stream()
-    upd_stream = torch.cuda.Stream() if args.overlap else stream  # default priority
+    # one stream per lane, default priority
+    streams = [stream] + [torch.cuda.Stream() for _ in range(job.lanes - 1)]
     nlaunch = w.decode_steps * job.R
 
     for i in range(args.warmup):
-        job.run(stream, upd_stream)
+        job.run(streams)
         torch.cuda.synchronize()
         log(f"warmup {i} done")
     job.check_errors()
 
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(w.decode_steps)] for _ in range(2)]
-    attn_ms = 0.0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        job.run(stream, upd_stream, events=ev)
-        torch.cuda.synchronize()
-        attn_ms += sum(a.elapsed_time(b) for a, b in zip(ev[0], ev[1]))
-        log(f"step {i} done")
+        job.run(streams)
+        log(f"step {i} issued")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    log("timed steps done")
     job.check_errors()
+
+    # the kernel's own launch duration: the same job once more on one
+    # stream, HIP events around each decode step's back-to-back launches
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(w.decode_steps)] for _ in range(2)]
+    job.run([stream], events=ev)
+    torch.cuda.synchronize()
+    attn_ms = sum(a.elapsed_time(b) for a, b in zip(ev[0], ev[1]))
+    job.check_errors()
+    log("single-stream pass done")
 
     ms_per_step = elapsed * 1e3 / args.steps
     tokens = job.R * w.batch * w.decode_steps
     value = tokens * args.steps / elapsed
     bytes_per_step = sum(job.decode_bytes(l) for l in job.len_sched) * job.R
-    avg_launch_us = attn_ms * 1e3 / (nlaunch * args.steps)
-    achieved = bytes_per_step * args.steps / (attn_ms * 1e-3) / 1e9
+    avg_launch_us = attn_ms * 1e3 / nlaunch
+    achieved = bytes_per_step / (attn_ms * 1e-3) / 1e9
     mean_bytes = bytes_per_step / nlaunch
+    overlapped = lanes_report(job, streams, rounds=8) if job.lanes > 1 else None
 
     result = {
         "metric": METRIC,
@@ -953,7 +1008,7 @@ def main():
                         f"decode-time merge every {w.merge_every} steps, {job.R} resident batches",
             "batch": w.batch, "prompt_len": w.prompt_len, "compacted_len": job.L0,
             "decode_steps": w.decode_steps, "resident_batches": job.R,
-            "update_overlap": bool(args.overlap),
+            "decode_lanes": job.lanes,
             "merge_first_stage": ("token table (sm_merge_token_table once, %.2f ms; sm_merge_spans_tabled per call)"
                                   % job.table_ms) if job.table is not None else "per call (sm_merge_spans)",
             "layer": {"d": w.d, "q_heads": w.num_q_heads, "kv_heads": w.num_kv_heads, "head_dim": w.head_dim},
@@ -961,7 +1016,8 @@ def main():
         },
         "roofline": {
             "kernel": "decode_split_bf16<128, step>: one fused append + attention launch per decode step and "
-                      "batch; HIP events around each step's back-to-back launches, divided by the launch count",
+                      "batch; HIP events around each step's back-to-back launches on one stream (a pass of the "
+                      "same job after the timed steps), divided by the launch count",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": PEAK_HBM_GBS,
@@ -972,6 +1028,8 @@ def main():
             "algorithmic_bytes_per_launch": int(mean_bytes),
         },
     }
+    if overlapped is not None:
+        result["roofline"]["overlapped"] = overlapped
     if not args.no_extras and args.decode_steps is None:
         try:
             result["extras"] = extras_report(job, stream, avg_launch_us)

@@ -295,3 +295,47 @@ def test_request_slots_and_duplicates(orc, n, dup):
         assert_same_state(c, oc)
     _counters_clear(ws)
     assert rel_l2_max(out.float().numpy(), ref) <= TOL[dtype]
+
+
+def test_steps_on_four_streams_match_the_oracle(orc):
+    """The benchmark's schedule: the resident batches' fused steps spread
+    over four streams (batch r on stream r % 4, one workspace per stream),
+    issued without host synchronisation so that launches of different
+    streams overlap.  Every step's output and the final cache states match
+    the oracle run step by step."""
+    dtype, Hq, H, D, bs = torch.bfloat16, 32, 8, 128, 16
+    R, NS, n, rounds = 8, 4, 16, 2
+    rng = np.random.RandomState(77)
+    caches = [_cache(orc, rng, dtype, H, D, bs, list(rng.randint(200, 900, size=n)), MB=64) for _ in range(R)]
+    ids = [rng.permutation(n) for _ in range(R)]
+    inputs = [[_inputs(rng, dtype, n, H, Hq, D) for _ in range(R)] for _ in range(rounds)]
+    max_len = 1000
+    streams = [torch.cuda.Stream() for _ in range(NS)]
+    wss = [torch.zeros(sm.decode_workspace_bytes(n, Hq, D, max_len), dtype=torch.uint8, device=dev())
+           for _ in range(NS)]
+    dev_in = [[tuple(x.to(dev()) for x in inputs[s][r]) for r in range(R)] for s in range(rounds)]
+    dev_ids = [i32(x) for x in ids]
+    outs = [[torch.full((n, Hq, D), float("nan"), dtype=dtype, device=dev()) for _ in range(R)]
+            for _ in range(rounds)]
+    torch.cuda.synchronize()
+    for st in streams:
+        st.wait_stream(torch.cuda.current_stream())
+    say("decode steps on", NS, "streams", R, "batches", rounds, "rounds")
+    for s in range(rounds):
+        for r in range(R):
+            K, V, q = dev_in[s][r]
+            sm.decode_step(caches[r][1], dev_ids[r], K, V, q, outs[s][r], wss[r % NS], max_len,
+                           stream=streams[r % NS])
+    torch.cuda.synchronize()
+    for s in range(rounds):
+        for r in range(R):
+            K, V, q = inputs[s][r]
+            st_a, st_d, ref = _oracle_step(orc, caches[r][0], ids[r], K, V, q, Hq)
+            assert st_a == orc.OK and st_d == orc.OK
+            e = rel_l2_max(outs[s][r].float().cpu().numpy(), ref)
+            assert e <= TOL[dtype], (s, r, e)
+    for oc, c in caches:
+        assert c.error_bits() == 0
+        assert_same_state(c, oc)
+    for ws in wss:
+        _counters_clear(ws)
