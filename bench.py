@@ -123,6 +123,15 @@ class Job:
         self.ids = i32(np.arange(B))
         self.one_row = i32(np.arange(B + 1))
         self.kreset = torch.empty(B, dtype=torch.int32, device=dev)
+        # prompt compression buffers per lane (lane 0's are the ones above),
+        # so that every lane compresses its own batches' prompts
+        self.cbuf = [dict(z=self.z, merge_ws=self.merge_ws, pi=self.pi, po=self.po, ps=self.ps,
+                          packed=self.packed, kreset=self.kreset)]
+        for _ in range(1, NL):
+            self.cbuf.append(dict(z=torch.empty_like(self.z), merge_ws=torch.empty_like(self.merge_ws),
+                                  pi=torch.empty_like(self.pi), po=torch.empty_like(self.po),
+                                  ps=torch.empty_like(self.ps), packed=torch.empty_like(self.packed),
+                                  kreset=torch.empty_like(self.kreset)))
         # decode-time merges: n per sequence per merge step, spans drawn from
         # a synthetic generated-token stream
         self.merge_steps = [s for s in range(steps) if w.merge_every and s % w.merge_every == w.merge_every - 1]
@@ -244,14 +253,13 @@ class Job:
     def run(self, streams, events=None):
         """One benchmark step: the whole job for every resident batch.
 
-        Lane l's batches (r % lanes == l) run their decode steps, and their
-        decode-time merges, in order on streams[l % len(streams)]; the lanes
-        share nothing, so their launches overlap: one lane's workgroups
-        stream their KV while the other's launch drains its last tiles and
-        combines.  Prompt compression runs on streams[0] (its buffers are
-        shared) after every lane's previous job, and the other lanes wait
-        for it.  With `events` (one stream only) each step's launches are
-        bracketed by events[0][s] and events[1][s]."""
+        Lane l's batches (r % lanes == l) run their prompt compression,
+        decode steps and decode-time merges, in order, on
+        streams[l % len(streams)]; the lanes share nothing, so their
+        launches overlap: one lane's workgroups stream their KV while
+        another's launch drains its last tiles and combines, or compresses
+        its prompts.  With `events` (one stream only) each step's launches
+        are bracketed by events[0][s] and events[1][s]."""
         import torch
         L, w = self.L, self.w
         B = w.batch
@@ -259,32 +267,30 @@ class Job:
         if events is not None and len(streams) != 1:
             raise ValueError("per-step events need a single stream")
         s0 = streams[0]
-        sb = s0.cuda_stream
         lane_st = [streams[l % len(streams)] for l in range(self.lanes)]
-        for st in streams[1:]:
-            s0.wait_stream(st)
-        # prompt compression of every batch (after its previous job's last
-        # decode step)
+        # prompt compression of every batch, on its lane (after its previous
+        # job's last decode step)
         for r in range(R):
             dp = self.dev_prompts[r]
             c = self.caches[r]
-            with torch.cuda.stream(s0):
-                self.kreset.copy_(c.lengths[:B])   # evict the previous job's sequences
-            rc = L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), self.kreset.data_ptr(), B, sb)
+            lane = r % self.lanes
+            cb, st = self.cbuf[lane], lane_st[lane]
+            sb = st.cuda_stream
+            with torch.cuda.stream(st):
+                cb["kreset"].copy_(c.lengths[:B])   # evict the previous job's sequences
+            rc = L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), cb["kreset"].data_ptr(), B, sb)
             rc |= self._merge_call(dp["row_idx"].data_ptr(), dp["rows"], dp["span_offsets"].data_ptr(), dp["S"],
-                                   self.z.data_ptr(), self.merge_ws, sb)
+                                   cb["z"].data_ptr(), cb["merge_ws"], sb)
             rc |= L.sm_pack_spans(B, dp["seq_offsets"].data_ptr(), B * w.prompt_len, dp["S"],
                                   dp["span_start"].data_ptr(), dp["span_len"].data_ptr(),
-                                  dp["seq_span_offsets"].data_ptr(), self.pi.data_ptr(), self.po.data_ptr(),
-                                  self.ps.data_ptr(), dp["token_ids"].data_ptr(), self.emb.data_ptr(),
-                                  self.emb.shape[0], self.z.data_ptr(), w.d, self.sm.SM_BF16, self.packed.data_ptr(),
-                                  self.err.data_ptr(), sb)
-            rc |= L.sm_kv_append(self.descs[r], self.ids.data_ptr(), self.po.data_ptr(), B, self.packed_rows[r],
+                                  dp["seq_span_offsets"].data_ptr(), cb["pi"].data_ptr(), cb["po"].data_ptr(),
+                                  cb["ps"].data_ptr(), dp["token_ids"].data_ptr(), self.emb.data_ptr(),
+                                  self.emb.shape[0], cb["z"].data_ptr(), w.d, self.sm.SM_BF16,
+                                  cb["packed"].data_ptr(), self.err.data_ptr(), sb)
+            rc |= L.sm_kv_append(self.descs[r], self.ids.data_ptr(), cb["po"].data_ptr(), B, self.packed_rows[r],
                                  self.Kp.data_ptr(), self.Vp.data_ptr(), sb)
             if rc:
                 raise RuntimeError(f"prompt compression launch failed: {rc}")
-        for st in streams[1:]:
-            st.wait_stream(s0)
         for s in range(w.decode_steps):
             if s in self.dmerge:
                 for lane, groups in enumerate(self.merge_groups):
