@@ -971,8 +971,9 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
+        t_issue = time.perf_counter()
         job.run(streams)
-        log(f"step {i} issued")
+        log(f"step {i} issued in {(time.perf_counter() - t_issue) * 1e3:.1f} ms of host time")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     log("timed steps done")
