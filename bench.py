@@ -313,9 +313,15 @@ def lanes_report(job, streams, rounds):
     """Fused decode steps of every resident batch back to back over the
     job's caches as the job left them, on one stream and then on the job's
     lanes: the rate at which the overlapped launches move the kernel's
-    algorithmic bytes.  Each round appends one row per sequence."""
+    algorithmic bytes.  Each round appends one row per sequence; every pass
+    rolls its rows back, so the caches end as the job left them.  Rounds
+    are limited by the caches' spare capacity (None if there is none)."""
     import torch
     w, B = job.w, job.w.batch
+    spare = job.max_len - max(int(c.lengths[:B].max()) for c in job.caches)
+    rounds = min(rounds, spare)
+    if rounds < 1:
+        return None
     res = {}
     for name, sts in (("one_stream", streams[:1]), ("lanes", streams)):
         lane_st = [sts[l % len(sts)] for l in range(job.lanes)]
@@ -334,14 +340,21 @@ def lanes_report(job, streams, rounds):
                 sts[0].wait_stream(st)
             e1.record(sts[0])
             torch.cuda.synchronize()
+            k = torch.full((B,), n, dtype=torch.int32, device=job.dev)
+            for r in range(job.R):
+                if job.L.sm_kv_rollback(job.descs[r], job.ids.data_ptr(), k.data_ptr(), B,
+                                        sts[0].cuda_stream):
+                    raise RuntimeError("roll back after the lanes measurement failed")
+            torch.cuda.synchronize()
         nbytes = sum(job.decode_bytes(lens0[r] + it + 1) for it in range(n) for r in range(job.R))
         us = e0.elapsed_time(e1) * 1e3 / (n * job.R)
         res[name] = {"us_per_launch": round(us, 3), "achieved": round(nbytes / (us * 1e-6 * n * job.R) / 1e9, 1)}
+        mean_len = float(lens0.mean()) + (n + 1) / 2
     job.check_errors()
     ach = res["lanes"]["achieved"]
     return {"lanes": job.lanes, "us_per_launch": res["lanes"]["us_per_launch"], "achieved": ach,
             "frac": round(ach / PEAK_HBM_GBS, 4), "one_stream_us_per_launch": res["one_stream"]["us_per_launch"],
-            "mean_cache_len": round(float(np.mean([c.lengths[:B].cpu().numpy() for c in job.caches])), 1),
+            "mean_cache_len": round(mean_len, 1),
             "note": "the fused step of every resident batch, %d rounds back to back over the job's caches, batch r "
                     "on stream r %% %d: bytes of all launches over the time from the first start to the last end; "
                     "overlapping launches have no duration of their own" % (rounds, job.lanes)}
