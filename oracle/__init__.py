@@ -21,20 +21,34 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# a test may point the wrapper at another build of the same source (the
+# sanitized one); nothing else sets this
+_LIB_OVERRIDE = os.environ.get("ORACLE_LIB")
 
 OK, EINVAL, ERANGE, ENOMEM = 0, 1, 2, 3
+
+
+_CFLAGS = ["-std=c11", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra", "-Wno-unused-parameter"]
 
 
 def build(force: bool = True) -> str:
     """Compile liboracle.so next to its source (gcc, -O2, OpenMP)."""
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
-               "-Wall", "-Wextra", "-Wno-unused-parameter",
-               _SRC, "-o", tmp, "-lm"]
+        cmd = ["gcc", "-O2", *_CFLAGS, _SRC, "-o", tmp, "-lm"]
         subprocess.run(cmd, check=True)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
+
+
+def build_sanitized(path: str) -> str:
+    """Compile the same source with AddressSanitizer and UndefinedBehavior-
+    Sanitizer (host code, gcc; any finding aborts) into ``path``.  A process
+    loads it through ORACLE_LIB with libasan preloaded."""
+    cmd = ["gcc", "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=all", *_CFLAGS, _SRC, "-o", path, "-lm"]
+    subprocess.run(cmd, check=True)
+    return path
 
 
 _lib = None
@@ -43,6 +57,10 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
+        if _LIB_OVERRIDE:
+            _lib = C.CDLL(_LIB_OVERRIDE)
+            _declare(_lib)
+            return _lib
         if not os.path.exists(_LIB_PATH):
             build()
         _lib = C.CDLL(_LIB_PATH)
