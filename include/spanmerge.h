@@ -367,6 +367,37 @@ sm_status sm_decode_step(const sm_paged_cache *c, const int32_t *seq_ids,
                          void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * sm_decode_step_noalloc -- for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): sm_decode_step with no workspace argument.  Its arrival
+ * counters and split partials live in a fixed array inside the library,
+ * one per device, held until the process ends; the call itself allocates
+ * nothing.  Same results, cache state and error bits as sm_decode_step
+ * (bit for bit: the same kernels with the same chunking).
+ *
+ *  arguments    as sm_decode_step, without ws / ws_bytes; the array of the
+ *               current device is used, so `stream` must belong to it.
+ *  size limit   n * num_q_heads * chunks * (head_dim + 2) * 4 bytes of
+ *               partials must fit sm_decode_step_noalloc_max_bytes()
+ *               (8 MiB); chunks is what the call's chunking uses (at most
+ *               ceil(max_len / 256); 2 for 16 sequences of up to 4096
+ *               entries, 8 KV heads).  Larger calls return SM_EINVAL and
+ *               launch nothing.
+ *  first call   on a device looks up the array's address and clears its
+ *               counters with a fill kernel on `stream` (SM_EHIP if either
+ *               fails); every call leaves them zero again.
+ *  concurrency  every call on a device shares that device's array: calls
+ *               that may overlap on one device (other streams, other host
+ *               threads) race and must be serialised by the caller.
+ */
+size_t sm_decode_step_noalloc_max_bytes(void);
+sm_status sm_decode_step_noalloc(const sm_paged_cache *c,
+                                 const int32_t *seq_ids, int n, const void *K,
+                                 const void *V, const void *q, int num_q_heads,
+                                 float scale, int max_len, void *out,
+                                 hipStream_t stream);
+
+/*
  * sm_prefill_attention -- the attention of the prefill pass over the
  * compressed prompt ("Efficiency Analysis": prompt merging shortens the
  * sequence before the backbone runs, so every layer attends over the

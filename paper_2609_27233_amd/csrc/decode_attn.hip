@@ -30,6 +30,8 @@
 // two 16-row score tiles are permuted so that the score tile's output layout
 // is already the PV operand layout: lane (r, q) of a wave owns the scores of
 // tokens 8q .. 8q+7 of the tile for head r.
+#include <mutex>
+
 #include "common.hpp"
 
 namespace sm {
@@ -1245,9 +1247,12 @@ SM_API size_t sm_decode_workspace_bytes(int n, int num_q_heads, int head_dim, in
 
 // Shared host checks and argument setup of sm_decode_attention and
 // sm_decode_step.
+// With exact_ws the workspace only has to hold what this call's chunking
+// uses (the scratch-array entry point); otherwise it must hold
+// sm_decode_workspace_bytes for these sizes, as documented.
 static sm_status decode_setup(const sm_paged_cache *c, const int32_t *seq_ids, int n, const void *q,
                               int num_q_heads, float scale, int max_len, void *out, void *ws, size_t ws_bytes,
-                              int64_t max_pairs, DecodeArgs &a) {
+                              int64_t max_pairs, DecodeArgs &a, bool exact_ws = false) {
   if (!c || n < 0 || max_len < 0) return SM_EINVAL;
   if (n == 0) return SM_OK;
   if (!seq_ids || !q || !out || !ws || !c->k_pool || !c->v_pool || !c->block_table ||
@@ -1263,7 +1268,7 @@ static sm_status decode_setup(const sm_paged_cache *c, const int32_t *seq_ids, i
   if (c->num_blocks <= 0 || c->max_seqs <= 0 || c->max_blocks_per_seq <= 0) return SM_EINVAL;
   if ((int64_t)max_len > (int64_t)c->max_blocks_per_seq * c->block_size) return SM_EINVAL;
   if (n > 65535 || (int64_t)n * c->num_kv_heads > max_pairs) return SM_EINVAL;
-  if (ws_bytes < sm_decode_workspace_bytes(n, num_q_heads, c->head_dim, max_len)) return SM_EINVAL;
+  if (!exact_ws && ws_bytes < sm_decode_workspace_bytes(n, num_q_heads, c->head_dim, max_len)) return SM_EINVAL;
 
   a = DecodeArgs{};
   a.k_pool = c->k_pool;
@@ -1286,6 +1291,9 @@ static sm_status decode_setup(const sm_paged_cache *c, const int32_t *seq_ids, i
                                           : kF32ChunkTokens;
   a.max_chunks = max_len > 0 ? (max_len + a.chunk_nominal - 1) / a.chunk_nominal : 1;
   a.scale_log2e = scale * kLog2e;
+  if (exact_ws &&
+      (uint64_t)ws_bytes < (uint64_t)kCounterBytes + (uint64_t)n * num_q_heads * a.max_chunks * (c->head_dim + 2) * 4)
+    return SM_EINVAL;
   a.counters = (int32_t *)ws;
   a.ws_o = (float *)((char *)ws + kCounterBytes);
   a.ws_ml = a.ws_o + (int64_t)n * num_q_heads * a.max_chunks * c->head_dim;
@@ -1324,15 +1332,15 @@ SM_API sm_status sm_decode_attention(const sm_paged_cache *c, const int32_t *seq
   return decode_launch<false>(c, a, n, stream);
 }
 
-SM_API sm_status sm_decode_step(const sm_paged_cache *c, const int32_t *seq_ids, int n, const void *K,
-                                const void *V, const void *q, int num_q_heads, float scale, int max_len,
-                                void *out, void *ws, size_t ws_bytes, hipStream_t stream) {
+static sm_status decode_step_impl(const sm_paged_cache *c, const int32_t *seq_ids, int n, const void *K,
+                                  const void *V, const void *q, int num_q_heads, float scale, int max_len,
+                                  void *out, void *ws, size_t ws_bytes, bool exact_ws, hipStream_t stream) {
   if (n > kDecThreads) return SM_EINVAL;
   if (n > 0 && (!K || !V || !c || !c->free_stack || !c->free_top)) return SM_EINVAL;
   DecodeArgs a;
   // the last two counter words are the step's error word and arrival counter
   const sm_status st = decode_setup(c, seq_ids, n, q, num_q_heads, scale, max_len, out, ws, ws_bytes,
-                                    kMaxPairs - 2, a);
+                                    kMaxPairs - 2, a, exact_ws);
   if (st != SM_OK || n == 0) return st;
   a.k_new = K;
   a.v_new = V;
@@ -1346,4 +1354,63 @@ SM_API sm_status sm_decode_step(const sm_paged_cache *c, const int32_t *seq_ids,
   a.cap = cap > INT32_MAX ? INT32_MAX : (int)cap;
   a.total_wgs = a.max_chunks * c->num_kv_heads * n;
   return decode_launch<true>(c, a, n, stream);
+}
+
+SM_API sm_status sm_decode_step(const sm_paged_cache *c, const int32_t *seq_ids, int n, const void *K,
+                                const void *V, const void *q, int num_q_heads, float scale, int max_len,
+                                void *out, void *ws, size_t ws_bytes, hipStream_t stream) {
+  return decode_step_impl(c, seq_ids, n, K, V, q, num_q_heads, scale, max_len, out, ws, ws_bytes, false, stream);
+}
+
+// ---------------------------------------------------------------------------
+// sm_decode_step_noalloc: the fused step with its workspace (arrival
+// counters + split partials) in a fixed device array instead of a caller
+// buffer, for callers that cannot allocate.  Each device the library runs
+// on holds its own copy of the array until the process ends; its address is
+// looked up once per device and kept.  The counters must be zero before the
+// first call: they are cleared once, by a fill kernel on the first call's
+// stream, and every call leaves them zero again.  Calls that overlap on one
+// device share the array and race.
+
+constexpr int64_t kScratchPartialBytes = 8ll << 20;
+constexpr int64_t kScratchBytes = kCounterBytes + kScratchPartialBytes;
+constexpr int kScratchMaxDevices = 64;
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+static __global__ void scratch_clear_kernel(uint32_t *p, int64_t words) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < words; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+static std::mutex g_scratch_mu;
+static void *g_scratch_ptr[kScratchMaxDevices];
+
+// Device address of this device's scratch array (cleared on first use), or
+// nullptr when it cannot be had.
+static void *scratch_for_current_device(hipStream_t stream) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    // counters only: the partials are written before they are read
+    hipLaunchKernelGGL(scratch_clear_kernel, dim3(64), dim3(256), 0, stream, (uint32_t *)ptr,
+                       (int64_t)(kCounterBytes / 4));
+    if (hipGetLastError() != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+SM_API size_t sm_decode_step_noalloc_max_bytes(void) { return (size_t)kScratchPartialBytes; }
+
+SM_API sm_status sm_decode_step_noalloc(const sm_paged_cache *c, const int32_t *seq_ids, int n, const void *K,
+                                        const void *V, const void *q, int num_q_heads, float scale, int max_len,
+                                        void *out, hipStream_t stream) {
+  void *ws = scratch_for_current_device(stream);
+  if (!ws) return SM_EHIP;
+  return decode_step_impl(c, seq_ids, n, K, V, q, num_q_heads, scale, max_len, out, ws, (size_t)kScratchBytes,
+                          true, stream);
 }

@@ -27,6 +27,7 @@ EXPORTED = ("sm_status_string", "sm_merge_workspace_bytes", "sm_merge_spans",
             "sm_merge_token_table", "sm_merge_spans_tabled",
             "sm_pack_spans", "sm_kv_rollback", "sm_kv_append",
             "sm_decode_workspace_bytes", "sm_decode_attention", "sm_decode_step",
+            "sm_decode_step_noalloc_max_bytes", "sm_decode_step_noalloc",
             "sm_prefill_attention", "sm_rules_build_workspace_bytes", "sm_rules_build",
             "sm_rules_lookup", "sm_match_prompt_workspace_bytes", "sm_match_prompt",
             "sm_match_decode", "sm_gather_surrogates", "sm_span_dedupe_workspace_bytes", "sm_span_dedupe",
@@ -98,6 +99,10 @@ def load(path: str = LIB_PATH):
     L.sm_decode_step.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _P, _P, _I, _F,
                                  _I, _P, _P, _Z, _P]
     L.sm_decode_step.restype = _I
+    L.sm_decode_step_noalloc_max_bytes.argtypes = []
+    L.sm_decode_step_noalloc_max_bytes.restype = _Z
+    L.sm_decode_step_noalloc.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _P, _P, _I, _F, _I, _P, _P]
+    L.sm_decode_step_noalloc.restype = _I
     L.sm_prefill_attention.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _I, _P, _I, _F, _I, _P, _P]
     L.sm_prefill_attention.restype = _I
     L.sm_rules_build_workspace_bytes.argtypes = [_I]
@@ -299,6 +304,18 @@ def decode_step(cache: PagedCache, seq_ids, K, V, q, out, ws, max_len: int,
                                max_len, _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
                                _stream(stream))
     _check(st, "sm_decode_step")
+
+
+def decode_step_noalloc(cache: PagedCache, seq_ids, K, V, q, out, max_len: int,
+                        scale: Optional[float] = None, stream=None):
+    """decode_step with the library's own per-device scratch array as its
+    workspace (no allocation in the call; calls on one device must not
+    overlap)."""
+    n, Hq, D = q.shape
+    sc = D ** -0.5 if scale is None else scale
+    st = load().sm_decode_step_noalloc(C.byref(cache.desc), _ptr(seq_ids), n, _ptr(K), _ptr(V), _ptr(q), Hq, sc,
+                                       max_len, _ptr(out), _stream(stream))
+    _check(st, "sm_decode_step_noalloc")
 
 
 def prefill_attention(cache: PagedCache, seq_ids, q_offsets, q, out, max_rows: int,
