@@ -442,22 +442,61 @@ def extras_report(job, stream, attn_us):
     del caches, descs, ws
     torch.cuda.empty_cache()
 
-    # --- cache operations on a fresh cache of the job's shape
+    out["cache_ops"] = cache_ops_report(job, stream)
+
+    out["merge_spans_70b_prompt_batch"] = merge_70b_report(job.sm, job.L, dev, stream)
+    out["prefill_attention"] = prefill_report(job.sm, job.L, dev, stream)
+    out["rule_matching"] = rules_report(job.sm, job.L, dev, stream)
+    out["surrogate_lookup"] = lut_report(job.sm, job.L, dev, stream)
+    out["kv_projection"] = kvproj_report(job.sm, job.L, dev, stream)
+    return out
+
+
+def _time_each(fn, undo, stream, reps):
+    """Average ms of fn() alone over reps calls, each bracketed by its own
+    HIP events on `stream`; undo() (untimed) runs after each call."""
+    import torch
+    fn()
+    undo()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for e0, e1 in evs:
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        undo()
+    torch.cuda.synchronize()
+    return sum(e0.elapsed_time(e1) for e0, e1 in evs) / reps
+
+
+def cache_ops_report(job, stream):
+    """The cache operations of one batch, as separate calls on a fresh cache
+    of the job's shape: the bulk append of a compressed prompt batch, pack,
+    the per-step append, rollback and a decode-time merge update."""
+    import torch
+    sm, L, w, dev = job.sm, job.L, job.w, job.dev
+    B, H, D, bs = w.batch, w.num_kv_heads, w.head_dim, w.block_size
+    st = stream.cuda_stream
+    ids = job.ids
     c = sm.PagedCache(dtype=w.torch_dtype, num_kv_heads=H, head_dim=D, block_size=bs,
                       num_blocks=job.caches[0].num_blocks, max_seqs=B,
                       max_blocks_per_seq=job.caches[0].max_blocks, device=dev)
     d = C.byref(c.desc)
     rows = job.packed_rows[0]
     kfull = torch.full((B,), job.L0, dtype=torch.int32, device=dev)
-
-    def bulk():
-        L.sm_kv_append(d, ids.data_ptr(), job.po.data_ptr(), B, rows, job.Kp.data_ptr(), job.Vp.data_ptr(), st)
-        L.sm_kv_rollback(d, ids.data_ptr(), kfull.data_ptr(), B, st)
     # packed offsets of batch 0 for the bulk append
     po = np.concatenate([[0], np.cumsum(np.full(B, job.L0))]).astype(np.int32)
     job.po.copy_(torch.as_tensor(po))
-    t_bulk_roll = _time(bulk, stream, 5)
-    L.sm_kv_append(d, ids.data_ptr(), job.po.data_ptr(), B, rows, job.Kp.data_ptr(), job.Vp.data_ptr(), st)
+
+    def bulk():
+        L.sm_kv_append(d, ids.data_ptr(), job.po.data_ptr(), B, rows, job.Kp.data_ptr(), job.Vp.data_ptr(), st)
+
+    def roll_all():
+        L.sm_kv_rollback(d, ids.data_ptr(), kfull.data_ptr(), B, st)
+    t_bulk = _time_each(bulk, roll_all, stream, 10)
+    t_bulk_roll = _time(lambda: (bulk(), roll_all()), stream, 5)
+    bulk()
+
     def step_append():
         L.sm_kv_append(d, ids.data_ptr(), job.one_row.data_ptr(), B, B, job.Kt[0].data_ptr(),
                        job.Vt[0].data_ptr(), st)
@@ -479,31 +518,30 @@ def extras_report(job, stream, attn_us):
                         job.po.data_ptr(), job.ps.data_ptr(), dp["token_ids"].data_ptr(), job.emb.data_ptr(),
                         job.emb.shape[0], job.z.data_ptr(), w.d, sm.SM_BF16, job.packed.data_ptr(),
                         job.err.data_ptr(), st)
-    t_pack = _time(pack, stream, 5)
+    t_pack = _time(pack, stream, 10)
     assert c.error_bits() == 0 and int(job.err.item()) == 0
     row_bytes = H * D * 2
-    out["cache_ops"] = {
+    append_bytes = 4 * rows * row_bytes                 # read and write of K and V
+    pack_bytes = 2 * rows * w.d * 2 + 8 * B * w.prompt_len
+    del c
+    torch.cuda.empty_cache()
+    log("cache operations done")
+    return {
         "bulk_append_rows": rows,
+        "bulk_append_us": round(t_bulk * 1e3, 2),
+        "bulk_append_GBps": round(append_bytes / (t_bulk * 1e-3) / 1e9, 1),
+        "bulk_append_frac": round(append_bytes / (t_bulk * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         "bulk_append_plus_full_rollback_ms": round(t_bulk_roll, 4),
-        "bulk_append_GBps": round(4 * rows * row_bytes / (t_bulk_roll * 1e-3) / 1e9, 1),
         "decode_append_16_rows_us": round(t_app * 1e3, 2),
         "rollback_16_seqs_k1_us": round(t_roll * 1e3, 2),
         "merge_update_16_seqs_us": round(t_mu * 1e3, 2),
         "pack_prompt_batch_us": round(t_pack * 1e3, 1),
-        "pack_GBps": round((2 * rows * w.d * 2 + 8 * B * w.prompt_len) / (t_pack * 1e-3) / 1e9, 1),
-        "note": "HIP events around back-to-back calls on one stream; merge update = roll back 3 entries and "
-                "append the surrogate's K/V for each of 16 sequences; "
-                "bytes: append reads and writes K and V, pack reads and writes the packed rows plus indices"}
-    log("extras: cache operations done")
-    del c
-    torch.cuda.empty_cache()
-
-    out["merge_spans_70b_prompt_batch"] = merge_70b_report(job.sm, job.L, dev, stream)
-    out["prefill_attention"] = prefill_report(job.sm, job.L, dev, stream)
-    out["rule_matching"] = rules_report(job.sm, job.L, dev, stream)
-    out["surrogate_lookup"] = lut_report(job.sm, job.L, dev, stream)
-    out["kv_projection"] = kvproj_report(job.sm, job.L, dev, stream)
-    return out
+        "pack_GBps": round(pack_bytes / (t_pack * 1e-3) / 1e9, 1),
+        "pack_frac": round(pack_bytes / (t_pack * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "note": "bulk append: HIP events around each call (metadata + copy launches), a full rollback between "
+                "calls; the rest: events around back-to-back calls on one stream; merge update = roll back 3 "
+                "entries and append the surrogate's K/V for each of 16 sequences; bytes: append reads and "
+                "writes K and V, pack reads and writes the packed rows plus 8 B of indices per token"}
 
 
 def merge_70b_report(sm, L, dev, stream, reps=3):
@@ -920,6 +958,8 @@ def main():
                     help="only time the surrogate lookup, the merge module on the same spans, and the dedupe")
     ap.add_argument("--rules-only", action="store_true",
                     help="only time the rule table build and the prompt / decode matching")
+    ap.add_argument("--cache-ops-only", action="store_true",
+                    help="only time the cache operations (bulk append, pack, step append, rollback) of one batch")
     ap.add_argument("--prefill-only", action="store_true",
                     help="only time the prefill attention over the compacted and uncompressed prompt batch")
     ap.add_argument("--no-token-table", action="store_true",
@@ -967,6 +1007,10 @@ def main():
         print(json.dumps(prefill_report(sm, sm.load(), dev, torch.cuda.current_stream())), flush=True)
         return
     w = wl.WORKLOADS[2]
+    if args.cache_ops_only:
+        job = Job(dataclasses.replace(w, decode_steps=128), 1, dev, token_table=False, lanes=1)
+        print(json.dumps(cache_ops_report(job, torch.cuda.current_stream())), flush=True)
+        return
     if args.decode_steps is not None:
         w = dataclasses.replace(w, decode_steps=args.decode_steps)
     job = Job(w, args.replicas, dev, token_table=not args.no_token_table, lanes=args.lanes)
