@@ -58,6 +58,22 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def decode_bytes(w, lens, fused=True):
+    """Algorithmic HBM bytes of one fused step launch ending at lengths
+    `lens`: K and V of every entry attended to (the cached ones from the
+    pool, the appended one from its input row), the appended rows' stores,
+    the queries, the outputs and the block table entries read (fused=False:
+    a plain attention launch, no stores)."""
+    es = 2 if w.dtype == "bf16" else 4
+    lens = np.asarray(lens, np.int64)
+    row = w.num_kv_heads * w.head_dim * es
+    kv = 2 * int(np.sum(lens)) * row
+    new_rows = 2 * len(lens) * row if fused else 0
+    qo = 2 * len(lens) * w.num_q_heads * w.head_dim * es
+    bt = 4 * int(np.sum(-(-lens // w.block_size)))
+    return kv + new_rows + qo + bt
+
+
 class Job:
     """Device state of R resident batches of one workload."""
 
@@ -195,19 +211,7 @@ class Job:
         self.descs = [C.byref(c.desc) for c in self.caches]
 
     def decode_bytes(self, lens, fused=True):
-        """Algorithmic HBM bytes of one fused step launch ending at lengths
-        `lens`: K and V of every entry attended to (the cached ones from the
-        pool, the appended one from its input row), the appended rows'
-        stores, the queries, the outputs and the block table entries read
-        (fused=False: a plain attention launch, no stores)."""
-        w = self.w
-        es = 2
-        row = w.num_kv_heads * w.head_dim * es
-        kv = 2 * int(np.sum(lens)) * row
-        new_rows = 2 * w.batch * row if fused else 0
-        qo = 2 * w.batch * w.num_q_heads * w.head_dim * es
-        bt = 4 * int(np.sum(-(-lens // w.block_size)))
-        return kv + new_rows + qo + bt
+        return decode_bytes(self.w, lens, fused)
 
     def _merge_call(self, row_idx, rows, offs, S, z, ws, st):
         """M_phi over one CSR batch of spans: from the token table when the
@@ -250,7 +254,7 @@ class Job:
         if rc:
             raise RuntimeError(f"decode step launch failed at step {s}: {rc}")
 
-    def run(self, streams, events=None):
+    def run(self, streams, events=None, hook=None):
         """One benchmark step: the whole job for every resident batch.
 
         Lane l's batches (r % lanes == l) run their prompt compression,
@@ -259,7 +263,11 @@ class Job:
         launches overlap: one lane's workgroups stream their KV while
         another's launch drains its last tiles and combines, or compresses
         its prompts.  With `events` (one stream only) each step's launches
-        are bracketed by events[0][s] and events[1][s]."""
+        are bracketed by events[0][s] and events[1][s].  `hook` (tests
+        only) is called after the prompt compression ("prompt", None),
+        after each merge step's merges ("merge", s) and after each decode
+        step's launches ("step", s); it may synchronize and read state, and
+        changes none of the launches."""
         import torch
         L, w = self.L, self.w
         B = w.batch
@@ -291,17 +299,23 @@ class Job:
                                  self.Kp.data_ptr(), self.Vp.data_ptr(), sb)
             if rc:
                 raise RuntimeError(f"prompt compression launch failed: {rc}")
+        if hook is not None:
+            hook("prompt", None)
         for s in range(w.decode_steps):
             if s in self.dmerge:
                 for lane, groups in enumerate(self.merge_groups):
                     for rs in groups:
                         self._merge(rs, s, lane, lane_st[lane].cuda_stream)
+                if hook is not None:
+                    hook("merge", s)
             if events is not None:
                 events[0][s].record(s0)
             for r in range(R):
                 self._step(r, s, lane_st[r % self.lanes].cuda_stream)
             if events is not None:
                 events[1][s].record(s0)
+            if hook is not None:
+                hook("step", s)
 
     def check_errors(self):
         bits = [c.error_bits() for c in self.caches] + [int(self.err.item())]
@@ -443,6 +457,7 @@ def extras_report(job, stream, attn_us):
     torch.cuda.empty_cache()
 
     out["cache_ops"] = cache_ops_report(job, stream)
+    out["configs"] = configs_report(dev, stream, (2, 3, 4, 5))
 
     out["merge_spans_70b_prompt_batch"] = merge_70b_report(job.sm, job.L, dev, stream)
     out["prefill_attention"] = prefill_report(job.sm, job.L, dev, stream)
@@ -542,6 +557,158 @@ def cache_ops_report(job, stream):
                 "calls; the rest: events around back-to-back calls on one stream; merge update = roll back 3 "
                 "entries and append the surrogate's K/V for each of 16 sequences; bytes: append reads and "
                 "writes K and V, pack reads and writes the packed rows plus 8 B of indices per token"}
+
+
+# resident replicas per configuration: R x (bytes per attention launch) is
+# at least 1 GiB, so no launch finds its cache in the 256 MB MALL
+CONFIG_REPLICAS = {2: 8, 3: 4, 4: 2, 5: 2}
+
+
+def config_start_lengths(w):
+    """Cached entries per sequence when decoding starts: the compressed
+    prompt length, or the seeded ragged contexts."""
+    if w.ctx_range is not None:
+        return wl_mod().context_lengths(w).astype(np.int64)
+    return np.full(w.batch, w.prompt_len - int(round(w.target * w.prompt_len)), np.int64)
+
+
+def wl_mod():
+    from paper_2609_27233_amd import workload as wl
+    return wl
+
+
+def config_decode_report(cid, dev, stream, reps=3, merge_every=None):
+    """Decode attention of one configuration at its full size: R resident
+    replicas of the batch's paged cache at the configuration's starting
+    lengths (random K/V; values do not change the traffic), then the
+    configuration's decode steps, each one fused append + attention launch
+    per replica (sm_decode_step), with the configuration's decode-time
+    rollback of k entries before every merge step (the appended row is
+    then the surrogate's).  Timed on one stream: tokens/s of the loop, and
+    the step kernel's launch duration from HIP events around each step's R
+    back-to-back launches."""
+    import dataclasses
+    import torch
+    from paper_2609_27233_amd import lib as sm
+    wl = wl_mod()
+    L = sm.load()
+    w = wl.WORKLOADS[cid]
+    if merge_every is not None:
+        w = dataclasses.replace(w, merge_every=merge_every)
+    B, H, D, Hq, bs = w.batch, w.num_kv_heads, w.head_dim, w.num_q_heads, w.block_size
+    dt = w.torch_dtype
+    R = CONFIG_REPLICAS[cid]
+    S = w.decode_steps
+    st = stream.cuda_stream
+    lens0 = config_start_lengths(w)
+    # host copy of the length schedule: k per merge step, lengths after each step
+    ks, sched = {}, []
+    lens = lens0.copy()
+    for s_ in range(S):
+        if w.merge_every and s_ % w.merge_every == w.merge_every - 1:
+            k = (wl.decode_merge_lengths(w, s_) - 1).astype(np.int64)
+            ks[s_] = k
+            lens = lens - k
+        lens = lens + 1
+        sched.append(lens.copy())
+    max_len = int(max(x.max() for x in sched))
+    peak = np.max(np.stack([lens0] + sched), axis=0)
+    nb_seq = -(-max_len // bs) + 1
+    NB = int(np.sum(-(-peak // bs))) + B
+    g = wl.generator(w.seed + 500, dev)
+    offs = torch.as_tensor(np.concatenate([[0], np.cumsum(lens0)]).astype(np.int32)).to(dev)
+    rows = int(lens0.sum())
+    K0 = wl.randn((rows, H, D), dt, g, device=dev)
+    V0 = wl.randn((rows, H, D), dt, g, device=dev)
+    ids = torch.arange(B, dtype=torch.int32, device=dev)
+    caches = []
+    for r in range(R):
+        c = sm.PagedCache(dtype=dt, num_kv_heads=H, head_dim=D, block_size=bs, num_blocks=NB, max_seqs=B,
+                          max_blocks_per_seq=nb_seq, device=dev,
+                          free_order=wl.free_order(NB, w.shuffled_pages, w.seed + r))
+        sm.kv_append(c, ids, offs, K0, V0, stream=stream)
+        caches.append(c)
+    del K0, V0
+    nin = 8
+    Kt = [wl.randn((B, H, D), dt, g, device=dev) for _ in range(nin)]
+    Vt = [wl.randn((B, H, D), dt, g, device=dev) for _ in range(nin)]
+    q = [wl.randn((B, Hq, D), dt, g, device=dev) for _ in range(nin)]
+    out = torch.empty((B, Hq, D), dtype=dt, device=dev)
+    ws = torch.zeros(sm.decode_workspace_bytes(B, Hq, D, max_len), dtype=torch.uint8, device=dev)
+    kdev = {s_: torch.as_tensor(k.astype(np.int32)).to(dev) for s_, k in ks.items()}
+    restore = torch.as_tensor((sched[-1] - lens0).astype(np.int32)).to(dev)
+    descs = [C.byref(c.desc) for c in caches]
+    scale = D ** -0.5
+    torch.cuda.synchronize()
+
+    def loop(ev=None):
+        for s_ in range(S):
+            if s_ in kdev:
+                for d in descs:
+                    L.sm_kv_rollback(d, ids.data_ptr(), kdev[s_].data_ptr(), B, st)
+            j = s_ % nin
+            if ev is not None:
+                ev[0][s_].record(stream)
+            for d in descs:
+                rc = L.sm_decode_step(d, ids.data_ptr(), B, Kt[j].data_ptr(), Vt[j].data_ptr(), q[j].data_ptr(), Hq,
+                                      scale, max_len, out.data_ptr(), ws.data_ptr(), ws.numel(), st)
+                if rc:
+                    raise RuntimeError(f"sm_decode_step failed at config {cid} step {s_}: {rc}")
+            if ev is not None:
+                ev[1][s_].record(stream)
+
+    def undo():
+        for d in descs:
+            L.sm_kv_rollback(d, ids.data_ptr(), restore.data_ptr(), B, st)
+
+    loop()
+    undo()
+    torch.cuda.synchronize()
+    elapsed, kern = [], []
+    for _ in range(reps):
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(S)] for _ in range(2)]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        loop(ev)
+        e1.record(stream)
+        undo()
+        torch.cuda.synchronize()
+        elapsed.append(e0.elapsed_time(e1))
+        kern.append(sum(a.elapsed_time(b) for a, b in zip(ev[0], ev[1])))
+    bad = [c.error_bits() for c in caches]
+    if any(bad):
+        raise RuntimeError(f"config {cid}: device error bits {bad}")
+    step_bytes = [decode_bytes(w, x) for x in sched]
+    t_loop = min(elapsed) * 1e-3
+    t_kern = min(kern) * 1e-3
+    launch_us = t_kern / (S * R) * 1e6
+    gbps = sum(step_bytes) * R / t_kern / 1e9
+    res = {
+        "workload": w.name, "batch": B, "q_heads": Hq, "kv_heads": H, "head_dim": D,
+        "start_len_mean": round(float(lens0.mean()), 1), "start_len_min": int(lens0.min()),
+        "start_len_max": int(lens0.max()), "end_len_mean": round(float(sched[-1].mean()), 1),
+        "decode_steps": S, "merge_every": w.merge_every, "replicas": R, "shuffled_pages": w.shuffled_pages,
+        "tokens_per_s": round(B * S * R / t_loop, 1),
+        "avg_launch_us": round(launch_us, 3),
+        "algorithmic_MB_per_launch": round(sum(step_bytes) / S / 1e6, 2),
+        "achieved_GBps": round(gbps, 1), "frac": round(gbps / PEAK_HBM_GBS, 4),
+        "note": "one stream; tokens/s = B x steps x replicas over the loop's time (best of %d), including the "
+                "rollback launches of the merge steps; launch time from HIP events around each step's "
+                "back-to-back launches" % reps}
+    del caches, ws
+    torch.cuda.empty_cache()
+    log(f"config {cid}: {res['avg_launch_us']} us per launch, {res['achieved_GBps']} GB/s")
+    return res
+
+
+def configs_report(dev, stream, cids=(3, 4, 5)):
+    out = {}
+    for cid in cids:
+        if cid == 2:
+            out["2_without_decode_merges"] = config_decode_report(2, dev, stream, merge_every=0)
+        else:
+            out[str(cid)] = config_decode_report(cid, dev, stream)
+    return out
 
 
 def merge_70b_report(sm, L, dev, stream, reps=3):
@@ -872,69 +1039,128 @@ def traffic_bytes(alg_bytes):
     return int(alg_bytes * TRAFFIC_RATIO)
 
 
-def cpu_baseline(job, target_s=20.0):
-    """Time the oracle on a bounded sample of one batch's job and scale it to
-    the whole job.  Sample: M_phi on 32 of the prompt spans (scaled to all
-    spans), pack + bulk append of one batch's prompt, and 2 decode steps
-    (append + attention) at the starting length (scaled to 256 steps)."""
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(job):
+    """The oracle (plain fp64 C, OpenMP) timed on this host's cores on a
+    bounded sample of one batch's job, scaled to the whole job.
+
+    Threads: len(os.sched_getaffinity(0)) (the cores this process may run
+    on).  Timed parts, on the job's own inputs:
+      (i)   decode attention (append one row per sequence, then attention)
+            of the full 16-sequence batch at the first decode step and at the
+            last step's lengths; the job's 256 steps are estimated from the
+            two by the step lengths (attention cost is linear in length);
+      (ii)  the merge module on a seeded sample of min(S, 2048) prompt spans,
+            extrapolated linearly to all S spans;
+      (iii) pack and bulk append of the batch's prompt (full size).
+    The decode-time merges (16 spans of 2-4 tokens every 8 steps) are
+    extrapolated from (ii) per span.  A one-thread figure repeats (i) at the
+    first step and (ii) on 64 spans."""
     import torch
     import oracle as orc
     from paper_2609_27233_amd import workload as wl
 
     w = job.w
     B, H, D, Hq = w.batch, w.num_kv_heads, w.head_dim, w.num_q_heads
+    threads = len(os.sched_getaffinity(0))
+    orc.set_num_threads(threads)
     P = job.prompts[0]
     S = len(P.span_len)
-    t_all = time.time()
-    # merge module on a sample of spans
-    ns = 1024
-    sample = np.arange(ns) * (S // ns)
-    offs = P.span_offsets
-    rows = np.concatenate([P.row_idx[offs[s]:offs[s + 1]] for s in sample])
-    uniq, inv = np.unique(rows, return_inverse=True)
-    emb_s = wl.to_f64(job.emb[torch.as_tensor(uniq, device=job.dev)])
-    so = np.concatenate([[0], np.cumsum([offs[s + 1] - offs[s] for s in sample])]).astype(np.int32)
     params = {k: wl.to_f64(v) for k, v in job.params.items()}
-    t = time.time()
-    st, _ = orc.merge_spans(emb_s, inv.astype(np.int32), so, params, w.h)
-    t_merge = (time.time() - t) * S / ns
-    assert st == 0
+    t_all = time.time()
+
+    def merge_time(ns, seed):
+        rng = np.random.RandomState(seed)
+        sample = np.sort(rng.choice(S, ns, replace=False))
+        offs = P.span_offsets
+        rows = np.concatenate([P.row_idx[offs[s_]:offs[s_ + 1]] for s_ in sample])
+        uniq, inv = np.unique(rows, return_inverse=True)
+        emb_s = wl.to_f64(job.emb[torch.as_tensor(uniq, device=job.dev)])
+        so = np.concatenate([[0], np.cumsum([offs[s_ + 1] - offs[s_] for s_ in sample])]).astype(np.int32)
+        t = time.time()
+        st, _ = orc.merge_spans(emb_s, inv.astype(np.int32), so, params, w.h)
+        assert st == 0
+        return (time.time() - t) / ns, float(np.mean(np.diff(so)))
+
+    ns = min(S, 2048)
+    t_span, mean_n = merge_time(ns, 11)
+    t_merge = t_span * S
     # pack of the whole batch (indices) and bulk append of its K/V
     t = time.time()
     st, res = orc.pack_spans(P.seq_offsets, P.span_start, P.span_len, P.seq_span_offsets)
     t_pack = time.time() - t
+    assert st == 0
     nb_seq = -(-job.max_len // w.block_size) + 2
     oc = orc.OracleCache(bf16=True, num_kv_heads=H, head_dim=D, block_size=w.block_size,
                          num_blocks=B * nb_seq, max_seqs=B, max_blocks_per_seq=nb_seq)
-    Kp, Vp = wl.to_raw(job.Kp), wl.to_raw(job.Vp)
     t = time.time()
-    st = oc.append(np.arange(B), res["packed_offsets"], Kp, Vp)
+    st = oc.append(np.arange(B), res["packed_offsets"], wl.to_raw(job.Kp), wl.to_raw(job.Vp))
     t_append = time.time() - t
     assert st == 0
-    # decode steps
-    nd = 24
     Kt, Vt = wl.to_raw(job.Kt[0]), wl.to_raw(job.Vt[0])
     q = wl.to_f64(job.q[0])
-    t = time.time()
-    for _ in range(nd):
-        oc.append(np.arange(B), np.arange(B + 1), Kt, Vt)
-        oc.decode_attention(np.arange(B), q, Hq, D ** -0.5)
-    t_dec = (time.time() - t) / nd
-    # attention cost grows with the cache: scale by the mean length over the job
+    ids = np.arange(B)
+
+    def step_time():
+        t = time.time()
+        assert oc.append(ids, np.arange(B + 1), Kt, Vt) == 0
+        assert oc.decode_attention(ids, q, Hq, D ** -0.5)[0] == 0
+        return time.time() - t
+
+    t_first = step_time()
+    # grow the cache to the last step's lengths (the job's schedule), then time that step
+    last = job.len_sched[-1]
+    grow = int(last.max()) - int(oc.lengths[:B].max()) - 1
+    for _ in range(max(grow, 0)):
+        oc.append(ids, np.arange(B + 1), Kt, Vt)
+    t_last = step_time()
+    first_len = float(job.L0 + 1)
+    last_len = float(np.mean(oc.lengths[:B]))
     mean_len = float(np.mean([np.mean(x) for x in job.len_sched]))
-    t_dec_job = t_dec * w.decode_steps * mean_len / (job.L0 + 1)
-    t_job = t_merge + t_pack + t_append + t_dec_job
+    slope = (t_last - t_first) / max(last_len - first_len, 1.0)
+    t_dec_job = w.decode_steps * (t_first + slope * (mean_len - first_len))
+    n_dec_spans = B * len(job.dmerge)
+    t_dec_merge = t_span * n_dec_spans * (3.0 / mean_n)   # decode-time spans hold 2-4 tokens (+ 1 output row)
+    t_job = t_merge + t_pack + t_append + t_dec_job + t_dec_merge
     tokens = B * w.decode_steps
+    measured = time.time() - t_all
+    # one thread: the first decode step and 64 spans
+    orc.set_num_threads(1)
+    t_span1, _ = merge_time(min(S, 64), 12)
+    oc.rollback(ids, np.full(B, int(oc.lengths[0]) - job.L0, np.int32))
+    t_first1 = step_time()
+    orc.set_num_threads(threads)
+    t_job1 = (t_span1 * S + t_pack + t_append * 1.0 + t_dec_job * t_first1 / t_first
+              + t_span1 * n_dec_spans * (3.0 / mean_n))
     return {
-        "value": tokens / t_job,
+        "value": round(tokens / t_job, 2),
         "unit": "tokens/s",
-        "cores": orc.num_threads(),
+        "cores": threads,
         "kind": "oracle",
-        "sample": (f"fp64 oracle on one 16-sequence batch: M_phi on {ns} of {S} prompt spans "
-                   f"(scaled x{S / ns:.0f}), full pack and bulk append ({job.packed_rows[0]} rows), "
-                   f"{nd} decode steps scaled to {w.decode_steps} by mean cache length; "
-                   f"job estimate {t_job:.1f}s from {time.time() - t_all:.1f}s measured"),
-        "seconds_measured": round(time.time() - t_all, 2),
+        "cpu_model": _cpu_model(),
+        "value_1_thread": round(tokens / t_job1, 3),
+        "sample": (f"fp64 oracle, {threads} threads (sched_getaffinity), on one 16-sequence batch of the job: "
+                   f"(i) append + attention of all 16 sequences at the first decode step ({t_first:.3f} s, "
+                   f"length {first_len:.0f}) and at the last step's lengths ({t_last:.3f} s, {last_len:.0f}), "
+                   f"256 steps estimated linearly in length; (ii) M_phi on {ns} of {S} prompt spans, "
+                   f"extrapolated to all spans and to the {n_dec_spans} decode-time spans; (iii) pack and "
+                   f"bulk append of the batch ({job.packed_rows[0]} rows, full size); job estimate "
+                   f"{t_job:.1f} s from {measured:.1f} s measured.  One thread: M_phi on 64 spans and the "
+                   f"first decode step ({t_first1:.3f} s), same scaling (pack/append as measured)"),
+        "parts_s": {"merge_prompt_extrapolated": round(t_merge, 2), "pack": round(t_pack, 3),
+                    "bulk_append": round(t_append, 3), "decode_steps": round(t_dec_job, 2),
+                    "decode_merges_extrapolated": round(t_dec_merge, 2)},
+        "seconds_measured": round(measured, 2),
     }
 
 
@@ -958,6 +1184,9 @@ def main():
                     help="only time the surrogate lookup, the merge module on the same spans, and the dedupe")
     ap.add_argument("--rules-only", action="store_true",
                     help="only time the rule table build and the prompt / decode matching")
+    ap.add_argument("--configs-only", type=str, default=None, metavar="IDS",
+                    help="only time the decode steps of these configurations (comma list of 2-5; 2 = without "
+                         "decode-time merges)")
     ap.add_argument("--cache-ops-only", action="store_true",
                     help="only time the cache operations (bulk append, pack, step append, rollback) of one batch")
     ap.add_argument("--prefill-only", action="store_true",
@@ -1005,6 +1234,10 @@ def main():
     if args.prefill_only:
         from paper_2609_27233_amd import lib as sm
         print(json.dumps(prefill_report(sm, sm.load(), dev, torch.cuda.current_stream())), flush=True)
+        return
+    if args.configs_only:
+        cids = tuple(int(x) for x in args.configs_only.split(","))
+        print(json.dumps(configs_report(dev, torch.cuda.current_stream(), cids)), flush=True)
         return
     w = wl.WORKLOADS[2]
     if args.cache_ops_only:

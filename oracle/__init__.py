@@ -124,6 +124,8 @@ def _declare(L):
     L.orc_kv_project.restype = _I
     L.orc_num_threads.argtypes = []
     L.orc_num_threads.restype = _I
+    L.orc_set_num_threads.argtypes = [_I]
+    L.orc_set_num_threads.restype = None
 
 
 def _ptr(a):
@@ -140,6 +142,10 @@ def _i32(a):
 
 def num_threads() -> int:
     return lib().orc_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    lib().orc_set_num_threads(int(n))
 
 
 # --------------------------------------------------------------------------
@@ -169,6 +175,53 @@ def merge_spans(emb, row_idx, span_offsets, params, h, ln_eps=1e-5, flags=0,
     if return_weights:
         return st, out, w
     return st, out
+
+
+def _gelu_erf(x):
+    from scipy.special import erf
+    return 0.5 * x * (1.0 + erf(x / np.sqrt(2.0)))
+
+
+def _layer_norm_rows(x, g, b, eps):
+    mean = x.mean(axis=-1, keepdims=True)
+    var = ((x - mean) ** 2).mean(axis=-1, keepdims=True)          # biased variance
+    return g * (x - mean) / np.sqrt(var + eps) + b
+
+
+def merge_spans_rows(emb, row_idx, span_offsets, params, h, ln_eps=1e-5):
+    """The same M_phi as merge_spans (appendix "Attention-based Pooling
+    Architecture"), for large calls: each of the two Linear layers is applied
+    to every row of the call as one float64 matrix product (each row's
+    Linear_kv, and each span's Linear_o, is independent of the others), so
+    the d x d weights stream once per call instead of once per row.  GELU,
+    LayerNorm over all d features and the per-head learned-query pooling
+    (P as key and value, scale 1/sqrt(d_h), head-major concatenation) follow
+    the definition element by element.  Returns float64 [S, d]."""
+    emb = np.asarray(emb, np.float64)
+    row_idx = _i32(row_idx)
+    offs = _i32(span_offsets)
+    p = {k: np.asarray(params[k], np.float64) for k in PARAM_NAMES}
+    d = emb.shape[1]
+    dh = d // h
+    S = len(offs) - 1
+    if S <= 0:
+        return np.zeros((0, d))
+    E = emb[row_idx]                                                # [R, d]
+    P = _layer_norm_rows(_gelu_erf(E @ p["W_kv"].T + p["b_kv"]), p["g_kv"], p["beta_kv"], ln_eps)
+    lens = np.diff(offs)
+    nmax = int(lens.max())
+    # spans padded to nmax rows; padded rows take no weight
+    idx = offs[:-1, None] + np.arange(nmax)[None, :]                 # [S, nmax]
+    valid = np.arange(nmax)[None, :] < lens[:, None]
+    Pp = P[np.where(valid, idx, 0)].reshape(S, nmax, h, dh)         # [S, nmax, h, dh]
+    sc = np.einsum("snhk,hk->snh", Pp, p["Q"]) / np.sqrt(dh)
+    sc = np.where(valid[:, :, None], sc, -np.inf)
+    sc = sc - sc.max(axis=1, keepdims=True)
+    a = np.exp(sc)
+    a = a / a.sum(axis=1, keepdims=True)                            # softmax over the span's rows
+    c = np.einsum("snh,snhk->shk", a, Pp).reshape(S, d)             # concat in head order
+    Y = _gelu_erf(c @ p["W_o"].T + p["b_o"])
+    return _layer_norm_rows(Y, p["g_o"], p["beta_o"], ln_eps)
 
 
 # --------------------------------------------------------------------------

@@ -46,6 +46,16 @@ int orc_num_threads(void) {
 #endif
 }
 
+/* Threads for the following parallel loops (timing only; results do not
+   depend on it: every loop writes disjoint outputs). */
+void orc_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------ */
 /* element access of raw pool storage                                       */
 

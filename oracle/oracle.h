@@ -167,5 +167,6 @@ int orc_kv_project(const orc_cache *c, const int32_t *seq_ids, int n,
 
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int orc_num_threads(void);
+void orc_set_num_threads(int n);
 
 #endif

@@ -23,14 +23,20 @@ pytestmark = pytest.mark.gpu
 
 def _merge_check(orc, emb, params, h, row_idx, offs, out, sample, tol):
     """Oracle M_phi on the sampled spans (with only the embedding rows they
-    use) against the GPU surrogates of those spans."""
+    use) against the GPU surrogates of those spans.  Large samples take the
+    oracle's batched-rows form (the same definition, weights streamed once
+    per call)."""
     used = np.unique(np.concatenate([row_idx[offs[s]:offs[s + 1]] for s in sample]))
     remap = {int(r): k for k, r in enumerate(used)}
     rows = np.array([remap[int(r)] for s in sample for r in row_idx[offs[s]:offs[s + 1]]], np.int32)
     so = np.concatenate([[0], np.cumsum([offs[s + 1] - offs[s] for s in sample])]).astype(np.int32)
     emb_used = wl.to_f64(emb[torch.as_tensor(used, device=emb.device)])
-    st, ref = orc.merge_spans(emb_used, rows, so, {k: wl.to_f64(v) for k, v in params.items()}, h)
-    assert st == orc.OK
+    p64 = {k: wl.to_f64(v) for k, v in params.items()}
+    if len(sample) > 64:
+        ref = orc.merge_spans_rows(emb_used, rows, so, p64, h)
+    else:
+        st, ref = orc.merge_spans(emb_used, rows, so, p64, h)
+        assert st == orc.OK
     e = rel_l2_max(out[torch.as_tensor(sample, device=out.device)].float().cpu().numpy(), ref)
     say("merge rel_l2_max over", len(sample), "spans:", e)
     assert e <= tol
@@ -72,6 +78,29 @@ class Lockstep:
         torch.cuda.synchronize()
         assert self.c.error_bits() == 0
         assert_same_state(self.c, self.oc, pools=pools)
+
+    def step(self, K, V, q, max_len, sample):
+        """One fused decode step on the GPU (sm_decode_step: append a row per
+        sequence, attend); the oracle appends, and attends for the sampled
+        sequences (every query head of each)."""
+        w = self.w
+        n = w.batch
+        if self.ws is None:
+            self.ws = torch.zeros(sm.decode_workspace_bytes(n, w.num_q_heads, w.head_dim, max_len),
+                                  dtype=torch.uint8, device=dev())
+        out = torch.empty((n, w.num_q_heads, w.head_dim), dtype=w.torch_dtype, device=dev())
+        sm.decode_step(self.c, i32(np.arange(n)), K.to(dev()), V.to(dev()), q.to(dev()), out, self.ws, max_len)
+        assert self.oc.append(np.arange(n), np.arange(n + 1), wl.to_raw(K), wl.to_raw(V)) == self.orc.OK
+        torch.cuda.synchronize()
+        assert self.c.error_bits() == 0
+        if len(sample):
+            st, ref = self.oc.decode_attention(sample, wl.to_f64(q[torch.as_tensor(sample)]), w.num_q_heads,
+                                               w.head_dim ** -0.5)
+            assert st == self.orc.OK
+            e = rel_l2_max(out[torch.as_tensor(sample, device=dev())].float().cpu().numpy(), ref)
+            assert e <= TOL[w.torch_dtype], e
+            return e
+        return 0.0
 
     def attention(self, q, max_len, sample):
         w = self.w
@@ -213,11 +242,70 @@ def test_config1_tiny_f32_full_chain(orc):
     ls.attention(torch.from_numpy(qn.astype(np.float32)), 1024, [0])
 
 
-@pytest.mark.parametrize("cid", [2, 3, 5])
-def test_prompt_compression_and_decode(orc, cid):
-    """Configs 2, 3, 5 at full size: all spans merged in one call (oracle on
-    a sample), pack and bulk append bit-exact, then decode steps with
-    decode-time merges (config 3 cadence) checked on sampled sequences."""
+def _full_decode(orc, w, ls, emb, params, g, steps, max_len, pool_every, seqs_per_step):
+    """The configuration's whole decode run with the fused step: every
+    decode-time merge's spans all checked, integer state after every step,
+    pools every `pool_every` steps, attention of every sequence at the first
+    step, every merge step and the last step, and of `seqs_per_step`
+    sampled sequences (every query head) at the others."""
+    rng = np.random.RandomState(w.seed + 31)
+    B, H, D = w.batch, w.num_kv_heads, w.head_dim
+    everyone = np.arange(B)
+    worst = 0.0
+    for s in range(steps):
+        merging = bool(w.merge_every) and s % w.merge_every == w.merge_every - 1
+        if merging:
+            n = wl.decode_merge_lengths(w, s)
+            offs = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+            row_idx = rng.randint(0, w.vocab, size=int(offs[-1])).astype(np.int32)
+            z = _gpu_merge(emb, row_idx, offs, params, w.h, w.torch_dtype)
+            _merge_check(orc, emb, params, w.h, row_idx, offs, z, everyone, TOL[w.torch_dtype])
+            ls.rollback(everyone, n - 1)
+        K = wl.randn((B, H, D), w.torch_dtype, g)
+        V = wl.randn((B, H, D), w.torch_dtype, g)
+        q = wl.randn((B, w.num_q_heads, D), w.torch_dtype, g)
+        full = merging or s == 0 or s == steps - 1
+        sample = everyone if full else np.sort(rng.choice(B, seqs_per_step, replace=False))
+        worst = max(worst, ls.step(K, V, q, max_len, sample))
+        ls.check_state(pools=(s % pool_every == pool_every - 1) or s == steps - 1)
+        if s % 32 == 31 or s == steps - 1:
+            say("step", s, "lengths", ls.oc.lengths[:4].tolist(), "worst attention rel_l2 so far", worst)
+
+
+def test_config2_prompt_compression_and_separate_decode_calls(orc):
+    """Config 2 at full size: all spans merged in one call (oracle on a
+    sample), pack and bulk append bit-exact, then 9 decode steps through the
+    separate append and attention calls, a decode-time merge at step 7.
+    (The benchmark's own job, with the fused step for all 256 steps, is
+    tests/test_gpu_job.py.)"""
+    w = wl.WORKLOADS[2]
+    P = wl.make_prompts(w)
+    g = wl.generator(w.seed, "cuda")
+    emb = wl.randn((w.vocab, w.d), w.torch_dtype, g, device="cuda", std=0.02)
+    params = wl.make_merge_params(w.d, w.h, w.torch_dtype, g, device="cuda")
+    S = len(P.span_len)
+    say("config 2", w.name, "spans", S, "rows", len(P.row_idx))
+    rng = np.random.RandomState(2)
+    merge_sample = np.unique(np.concatenate([[0, S - 1], rng.choice(S, 254, replace=False)]))
+    L0 = w.prompt_len - int(round(w.target * w.prompt_len))
+    steps = 9
+    max_len = L0 + steps
+    nb_seq = -(-max_len // w.block_size) + 2
+    NB = w.batch * nb_seq
+    ls = Lockstep(orc, w, NB, nb_seq, free_order=wl.free_order(NB, w.shuffled_pages, w.seed))
+    gk = wl.generator(w.seed + 3)
+    _prompt_phase(orc, w, ls, P, emb, params, gk, merge_sample)
+    attn_sample = np.sort(rng.choice(w.batch, 4, replace=False))
+    _decode_phase(orc, w, ls, emb, params, gk, steps, max_len, attn_sample, check_every=4, merge_sample_size=4)
+
+
+@pytest.mark.parametrize("cid", [3, 5])
+def test_prompt_compression_and_full_decode(orc, cid):
+    """Configs 3 and 5 at full size for their whole runs: every prompt span
+    merged in one call (1024 sampled spans plus the first and last checked),
+    pack and bulk append bit-exact, then all decode steps (128 with a
+    decode-time merge every 8 steps for config 3, 64 for config 5) with the
+    fused step; at least 64 (sequence, head) rows checked per step."""
     w = wl.WORKLOADS[cid]
     P = wl.make_prompts(w)
     g = wl.generator(w.seed, "cuda")
@@ -226,31 +314,31 @@ def test_prompt_compression_and_decode(orc, cid):
     S = len(P.span_len)
     say("config", cid, w.name, "spans", S, "rows", len(P.row_idx))
     rng = np.random.RandomState(cid)
-    merge_sample = np.unique(np.concatenate([[0, S - 1], rng.choice(S, 14, replace=False)]))
+    merge_sample = np.unique(np.concatenate([[0, S - 1], rng.choice(S, 1024, replace=False)]))
     L0 = w.prompt_len - int(round(w.target * w.prompt_len))
-    steps = 9
+    steps = w.decode_steps
     max_len = L0 + steps
     nb_seq = -(-max_len // w.block_size) + 2
     NB = w.batch * nb_seq
-    order = wl.free_order(NB, w.shuffled_pages, w.seed)
-    ls = Lockstep(orc, w, NB, nb_seq, free_order=order)
+    ls = Lockstep(orc, w, NB, nb_seq, free_order=wl.free_order(NB, w.shuffled_pages, w.seed))
     gk = wl.generator(w.seed + 3)
     _prompt_phase(orc, w, ls, P, emb, params, gk, merge_sample)
-    attn_sample = np.arange(w.batch) if w.batch <= 4 else np.sort(rng.choice(w.batch, 4, replace=False))
-    wd = w if w.merge_every else __import__("dataclasses").replace(w, merge_every=8)
-    _decode_phase(orc, wd, ls, emb, params, gk, steps, max_len, attn_sample, check_every=4, merge_sample_size=4)
+    _full_decode(orc, w, ls, emb, params, gk, steps, max_len, pool_every=32 if cid == 3 else 16,
+                 seqs_per_step=-(-64 // w.num_q_heads))
 
 
 def test_config4_ragged_contexts_with_frequent_rollback(orc):
-    """Config 4: 128 sequences with contexts uniform in [512, 4096], a
-    decode-time merge (k ~ U{2,3,4}, n = k + 1 tokens at d = 3584) every 4
-    steps, attention over the ragged cache."""
+    """Config 4: 128 sequences with contexts uniform in [512, 4096], all 256
+    decode steps with the fused step, a decode-time merge (k ~ U{2,3,4},
+    n = k + 1 tokens at d = 3584, all 128 spans checked) and rollback every
+    4 steps, attention over the ragged cache (3 sequences x 28 heads per
+    step, every sequence at merge steps and the first and last)."""
     w = wl.WORKLOADS[4]
     lens = wl.context_lengths(w)
     g = wl.generator(w.seed, "cuda")
     emb = wl.randn((w.vocab, w.d), w.torch_dtype, g, device="cuda", std=0.02)
     params = wl.make_merge_params(w.d, w.h, w.torch_dtype, g, device="cuda")
-    steps = 9
+    steps = w.decode_steps
     max_len = int(lens.max()) + steps
     nb_seq = -(-max_len // w.block_size) + 2
     NB = int(np.sum(-(-(lens + steps) // w.block_size))) + w.batch + 8
@@ -262,8 +350,5 @@ def test_config4_ragged_contexts_with_frequent_rollback(orc):
     V = wl.randn((int(offs[-1]), w.num_kv_heads, w.head_dim), w.torch_dtype, gk)
     ls.append(np.arange(w.batch), offs, K, V)
     ls.check_state()
-    rng = np.random.RandomState(4)
-    attn_sample = np.sort(np.concatenate([[int(np.argmin(lens)), int(np.argmax(lens))],
-                                          rng.choice(w.batch, 4, replace=False)]))
-    _decode_phase(orc, w, ls, emb, params, gk, steps, max_len, np.unique(attn_sample), check_every=4,
-                  merge_sample_size=6)
+    del K, V
+    _full_decode(orc, w, ls, emb, params, gk, steps, max_len, pool_every=32, seqs_per_step=3)

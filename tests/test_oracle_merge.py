@@ -171,3 +171,28 @@ def test_rejects_bad_spans(orc):
     emb = np.zeros((4, d))
     assert orc.merge_spans(emb, np.array([0, 9], np.int32), np.array([0, 2], np.int32), p, h)[0] == orc.EINVAL
     assert orc.merge_spans(emb, np.array([0, 1], np.int32), np.array([0, 0, 2], np.int32), p, h)[0] == orc.EINVAL
+
+
+@pytest.mark.parametrize("d,h,spread", [(64, 4, True), (256, 4, False), (96, 3, True)])
+def test_rows_form_matches_the_c_oracle_and_torch(orc, d, h, spread):
+    """The batched-rows form used for full-size samples equals the C oracle
+    span by span, and the torch library composition."""
+    rng = np.random.RandomState(3 * d + h)
+    emb = rng.normal(0, 0.5, size=(40, d))
+    p = _params(d, h, seed=d + 1, spread=spread)
+    row_idx, offs = _spans(rng, 20, 8, 40)
+    offs = np.asarray(offs, np.int32)
+    st, out = orc.merge_spans(emb, row_idx, offs, p, h)
+    assert st == orc.OK
+    rows = orc.merge_spans_rows(emb, row_idx, offs, p, h)
+    np.testing.assert_allclose(rows, out, rtol=1e-11, atol=1e-11)
+    for s in (0, 7, len(offs) - 2):
+        np.testing.assert_allclose(rows[s], _torch_merge(emb[row_idx[offs[s]:offs[s + 1]]], p, h),
+                                   rtol=1e-11, atol=1e-11)
+    # a single-row span takes the whole weight; permuting a span's rows changes nothing
+    one = orc.merge_spans_rows(emb, row_idx[:1], np.array([0, 1], np.int32), p, h)
+    np.testing.assert_allclose(one[0], _torch_merge(emb[row_idx[:1]], p, h), rtol=1e-11, atol=1e-11)
+    a, b = offs[3], offs[4]
+    perm = row_idx.copy()
+    perm[a:b] = perm[a:b][::-1]
+    np.testing.assert_allclose(orc.merge_spans_rows(emb, perm, offs, p, h)[3], rows[3], rtol=1e-11, atol=1e-12)
