@@ -36,7 +36,9 @@
  * ----------------------------
  *  - Every pointer is a DEVICE pointer unless its comment says (host).
  *  - The caller owns every buffer (tables, pools, workspaces, outputs); the
- *    library allocates nothing, keeps no global state and never synchronizes.
+ *    library allocates nothing and never synchronizes.  Its only state: the
+ *    per-device scratch array of sm_decode_step_noalloc and the test-only
+ *    bound of sm_set_commit_wait_limit.
  *    Work is enqueued on `stream` (0 = the null stream); pointers must stay
  *    valid until that work has completed.  Calls are safe to capture in a
  *    HIP graph.
@@ -365,6 +367,19 @@ sm_status sm_decode_step(const sm_paged_cache *c, const int32_t *seq_ids,
                          int n, const void *K, const void *V, const void *q,
                          int num_q_heads, float scale, int max_len, void *out,
                          void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * sm_set_commit_wait_limit -- for tests of a fused step's give-up path (not
+ * for production use).  A fused step's append is committed by one extra
+ * workgroup once every attention workgroup has read the metadata; it polls
+ * for that at most `polls` times (default 2^20, restored by polls <= 0),
+ * which always suffices because every attention workgroup arrives without
+ * waiting on anything.  If the bound is reached anyway, the call commits
+ * nothing, sets EINVAL in c->err, and leaves the workspace's arrival counter
+ * nonzero: zero the first 256 KiB of that workspace again before reusing it.
+ * Process-wide; takes effect for calls issued after it returns.
+ */
+void sm_set_commit_wait_limit(int polls);
 
 /*
  * sm_decode_step_noalloc -- for callers that cannot allocate device memory

@@ -30,6 +30,7 @@
 // two 16-row score tiles are permuted so that the score tile's output layout
 // is already the PV operand layout: lane (r, q) of a wave owns the scores of
 // tokens 8q .. 8q+7 of the tile for head r.
+#include <atomic>
 #include <mutex>
 
 #include "common.hpp"
@@ -68,6 +69,7 @@ struct DecodeArgs {
   int32_t *step_err;         // workspace word: error bits parked until commit
   int32_t *step_arrivals;    // workspace word: workgroups past their reads
   int n, cap, total_wgs;
+  int spin_limit;            // polls of the commit workgroup's bounded wait
 };
 
 // Chunking of a sequence of L cached entries: nc non-empty chunks of
@@ -516,7 +518,11 @@ __device__ __forceinline__ int request_value(const int (&v)[4], int i) {
 // -- bounded, sleeping -- until every attention workgroup has taken its
 // reads of the metadata, then the metadata writes and the error bits.
 // Every attention workgroup arrives exactly once, early, and nothing waits
-// on this workgroup, so the wait ends; the bound only guards the invariant.
+// on this workgroup, so the wait ends; the bound (a.spin_limit polls) only
+// guards the invariant.  If it ever gives up, nothing is committed and
+// EINVAL is set; workgroups still arriving then leave the arrival counter
+// nonzero, so the caller must zero the workspace's counters again before
+// its next call.  (A lower bound can be set for tests of this path.)
 constexpr int kCommitSpinLimit = 1 << 20;
 
 __device__ void step_commit_wave(const DecodeArgs &a) {
@@ -528,7 +534,7 @@ __device__ void step_commit_wave(const DecodeArgs &a) {
   plan_any(a, pr, po);
   int arrived = 0;
   if (lane == 0) {
-    for (int it = 0; it < kCommitSpinLimit; ++it) {
+    for (int it = 0; it < a.spin_limit; ++it) {
       if (__hip_atomic_load(a.step_arrivals, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= a.total_wgs) {
         arrived = 1;
         break;
@@ -1333,6 +1339,14 @@ SM_API sm_status sm_decode_attention(const sm_paged_cache *c, const int32_t *seq
   return decode_launch<false>(c, a, n, stream);
 }
 
+// Polls of the fused step's commit wait (kCommitSpinLimit unless a test
+// lowers it to exercise the give-up path).
+static std::atomic<int> g_commit_spin_limit{kCommitSpinLimit};
+
+SM_API void sm_set_commit_wait_limit(int polls) {
+  g_commit_spin_limit.store(polls > 0 ? polls : kCommitSpinLimit);
+}
+
 static sm_status decode_step_impl(const sm_paged_cache *c, const int32_t *seq_ids, int n, const void *K,
                                   const void *V, const void *q, int num_q_heads, float scale, int max_len,
                                   void *out, void *ws, size_t ws_bytes, bool exact_ws, hipStream_t stream) {
@@ -1354,6 +1368,7 @@ static sm_status decode_step_impl(const sm_paged_cache *c, const int32_t *seq_id
   const int64_t cap = (int64_t)c->max_blocks_per_seq * c->block_size;
   a.cap = cap > INT32_MAX ? INT32_MAX : (int)cap;
   a.total_wgs = a.max_chunks * c->num_kv_heads * n;
+  a.spin_limit = g_commit_spin_limit.load();
   return decode_launch<true>(c, a, n, stream);
 }
 

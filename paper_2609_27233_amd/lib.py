@@ -27,7 +27,7 @@ EXPORTED = ("sm_status_string", "sm_merge_workspace_bytes", "sm_merge_spans",
             "sm_merge_token_table", "sm_merge_spans_tabled",
             "sm_pack_spans", "sm_kv_rollback", "sm_kv_append",
             "sm_decode_workspace_bytes", "sm_decode_attention", "sm_decode_step",
-            "sm_decode_step_noalloc_max_bytes", "sm_decode_step_noalloc",
+            "sm_decode_step_noalloc_max_bytes", "sm_decode_step_noalloc", "sm_set_commit_wait_limit",
             "sm_prefill_attention", "sm_rules_build_workspace_bytes", "sm_rules_build",
             "sm_rules_lookup", "sm_match_prompt_workspace_bytes", "sm_match_prompt",
             "sm_match_decode", "sm_gather_surrogates", "sm_span_dedupe_workspace_bytes", "sm_span_dedupe",
@@ -103,6 +103,8 @@ def load(path: str = LIB_PATH):
     L.sm_decode_step_noalloc_max_bytes.restype = _Z
     L.sm_decode_step_noalloc.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _P, _P, _I, _F, _I, _P, _P]
     L.sm_decode_step_noalloc.restype = _I
+    L.sm_set_commit_wait_limit.argtypes = [_I]
+    L.sm_set_commit_wait_limit.restype = None
     L.sm_prefill_attention.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _I, _P, _I, _F, _I, _P, _P]
     L.sm_prefill_attention.restype = _I
     L.sm_rules_build_workspace_bytes.argtypes = [_I]

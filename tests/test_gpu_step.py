@@ -339,3 +339,43 @@ def test_steps_on_four_streams_match_the_oracle(orc):
         assert_same_state(c, oc)
     for ws in wss:
         _counters_clear(ws)
+
+
+def test_commit_wait_give_up_commits_nothing_and_reports_einval(orc):
+    """The commit workgroup's bounded wait, forced from the host to give up
+    after one poll (every kernel still exits normally: nothing waits on the
+    commit workgroup): EINVAL, no metadata change, the logical cache intact.
+    After the workspace counters are zeroed again and the error word
+    cleared, the next step matches the oracle, which never saw the failed
+    call."""
+    dtype, Hq, H, D, bs = torch.bfloat16, 32, 8, 128, 16
+    rng = np.random.RandomState(77)
+    lens = [4000] * 16
+    oc, c = _cache(orc, rng, dtype, H, D, bs, lens)
+    ids = np.arange(len(lens))
+    max_len = max(lens) + 8
+    snap = _snapshot(c)
+    K, V, q = _inputs(rng, dtype, len(ids), H, Hq, D)
+    L = sm.load()
+    say("commit wait forced to give up")
+    L.sm_set_commit_wait_limit(1)
+    try:
+        _, ws = _gpu_step(c, ids, K, V, q, max_len)
+    finally:
+        L.sm_set_commit_wait_limit(0)
+    assert c.error_bits() == sm.ERR_EINVAL
+    for k in ("lengths", "block_table", "free_top"):
+        assert torch.equal(getattr(c, k), snap[k]), k
+    top = int(c.free_top.item())
+    assert torch.equal(c.free_stack[:top], snap["free_stack"][:top])
+    ws.zero_()
+    c.clear_error()
+    K, V, q = _inputs(rng, dtype, len(ids), H, Hq, D)
+    st_a, st_d, ref = _oracle_step(orc, oc, ids, K, V, q, Hq)
+    assert st_a == orc.OK and st_d == orc.OK
+    out, _ = _gpu_step(c, ids, K, V, q, max_len, ws)
+    assert c.error_bits() == 0
+    assert_same_state(c, oc, pools=False)
+    e = rel_l2_max(out.float().numpy(), ref)
+    say("step after the give-up: rel_l2_max", e)
+    assert e <= TOL[dtype]
