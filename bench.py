@@ -374,6 +374,59 @@ def lanes_report(job, streams, rounds):
                     "overlapping launches have no duration of their own" % (rounds, job.lanes)}
 
 
+def graph_report(job, rounds):
+    """The fused step of every resident batch, R launches back to back on one
+    stream, captured once as a HIP graph and replayed `rounds` times (each
+    replay appends one row per sequence; the rows are rolled back
+    afterwards), against the same launches issued eagerly: the time per
+    launch including the gaps between launches.  None if the caches have no
+    spare capacity."""
+    import torch
+    w, B = job.w, job.w.batch
+    spare = job.max_len - max(int(c.lengths[:B].max()) for c in job.caches)
+    rounds = min(rounds, spare // 2)
+    if rounds < 1:
+        return None
+    stream = torch.cuda.Stream()
+    res = {}
+    with torch.cuda.stream(stream):
+        torch.cuda.synchronize()
+        lens0 = [c.lengths[:B].clone() for c in job.caches]
+        # eager, one stream
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(rounds):
+            for r in range(job.R):
+                job._step(r, 0, stream.cuda_stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        res["eager_us_per_launch"] = round(e0.elapsed_time(e1) * 1e3 / (rounds * job.R), 3)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for r in range(job.R):
+                job._step(r, 0, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(rounds - 1):
+            g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        res["graph_us_per_launch"] = round(e0.elapsed_time(e1) * 1e3 / ((rounds - 1) * job.R), 3) if rounds > 1 \
+            else None
+        for r, c in enumerate(job.caches):
+            grown = (c.lengths[:B] - lens0[r]).to(torch.int32).contiguous()
+            if int(grown.min()) != 2 * rounds - 1 or int(grown.max()) != 2 * rounds - 1:
+                raise RuntimeError("graph replays did not append one row per sequence each")
+            if job.L.sm_kv_rollback(job.descs[r], job.ids.data_ptr(), grown.data_ptr(), B, stream.cuda_stream):
+                raise RuntimeError("roll back after the graph measurement failed")
+        torch.cuda.synchronize()
+    job.check_errors()
+    res["rounds"] = rounds
+    res["note"] = ("one decode step of all %d resident batches (R fused launches) on one stream: eager issue "
+                   "against one captured HIP graph replayed; HIP events around all rounds" % job.R)
+    return res
+
+
 def _time(fn, stream, reps):
     """Average ms of fn() over reps calls, HIP events on `stream`."""
     import torch
@@ -1286,6 +1339,7 @@ def main():
     achieved = bytes_per_step / (attn_ms * 1e-3) / 1e9
     mean_bytes = bytes_per_step / nlaunch
     overlapped = lanes_report(job, streams, rounds=8) if job.lanes > 1 else None
+    graph = graph_report(job, rounds=16)
 
     result = {
         "metric": METRIC,
@@ -1327,6 +1381,8 @@ def main():
     }
     if overlapped is not None:
         result["roofline"]["overlapped"] = overlapped
+    if graph is not None:
+        result["roofline"]["graph"] = graph
     if not args.no_extras and args.decode_steps is None:
         try:
             result["extras"] = extras_report(job, stream, avg_launch_us)
