@@ -69,7 +69,10 @@ struct DecodeArgs {
   int32_t *step_err;         // workspace word: error bits parked until commit
   int32_t *step_arrivals;    // workspace word: workgroups past their reads
   int n, cap, total_wgs;
-  int spin_limit;            // polls of the commit workgroup's bounded wait
+  int spin_limit;            // polls of the commit workgroup's bounded wait  // bf16 kernels, one chunk per (sequence, kv head): with order_n > 0 the
+  // grid's workgroups take the (sequence, head) pairs longest first, dealt
+  // over order_cus compute units holding order_occ workgroups each
+  int order_n, order_cus, order_occ;
 };
 
 // Chunking of a sequence of L cached entries: nc non-empty chunks of
@@ -83,13 +86,71 @@ __device__ __forceinline__ void chunking(int L, int C, int &nc, int &chunk) {
 
 // Sequence-level checks shared by split and combine.  Returns 0 when the
 // sequence can be processed, else the error bit (0 length is fine).
-__device__ __forceinline__ int seq_status(const DecodeArgs &a, int s, int &L) {
+__device__ __forceinline__ int seq_status(const DecodeArgs &a, int s, int &L, bool known = false,
+                                          int L_known = 0) {
   L = 0;
   if (s < 0 || s >= a.max_seqs) return SM_ERR_EINVAL;
-  L = a.lengths[s];
+  L = known ? L_known : a.lengths[s];
   if (L < 0 || L > (a.max_blocks << a.bs_log2)) return SM_ERR_EINVAL;
   if (L > a.max_len) return SM_ERR_ERANGE;
   return 0;
+}
+
+// Ragged batches with more (sequence, kv head) pairs than compute units
+// (one chunk each): every workgroup sorts the requests by cached length
+// (longest first, ties by request index) and takes the pair of its rank, so
+// that long pairs start first.  While the grid's first order_occ *
+// order_cus workgroups are all resident, workgroup b shares a compute unit
+// with b +- order_cus (the dispatcher deals one per unit in grid order), so
+// alternate rounds of order_cus ranks are dealt in reverse: a unit that
+// got a long pair in one round gets a short one in the next.  Workgroups
+// past that point are dispatched as units free up, longest first.  The
+// order only decides which workgroup does which pair: results do not
+// depend on it.
+__device__ __forceinline__ int dealt_rank(int b, int W, int cus, int occ) {
+  const int M = min(W, cus * occ);
+  if (b >= M || cus <= 0) return b;
+  const int r = b / cus;
+  if (!(r & 1)) return b;
+  const int mr = min(cus, M - r * cus);
+  return r * cus + (mr - 1 - (b - r * cus));
+}
+
+// The (request, kv head) of grid position (row i, head column g) under the
+// length order; s_out / L_out: the request's sequence id and its cached
+// length (-1 for an id out of range).  All threads take part: order_n is at
+// most the workgroup size, one request per thread.  `key` holds order_n
+// ints of LDS, `pick` three.
+__device__ __forceinline__ void order_pick(const DecodeArgs &a, int &g, int &i, int &s_out, int &L_out,
+                                           int *key, int *pick) {
+  const int n = a.order_n, tid = threadIdx.x;
+  const int rho = dealt_rank(i * a.Hkv + g, n * a.Hkv, a.order_cus, a.order_occ);
+  const int k = rho / a.Hkv;
+  g = rho - k * a.Hkv;
+  int sj = -1, kj = -1;
+  if (tid < n) {
+    sj = a.seq_ids[tid];
+    kj = (sj >= 0 && sj < a.max_seqs) ? a.lengths[sj] : -1;
+    key[tid] = kj;
+  }
+  lds_barrier();
+  if (tid < n) {
+    int r = 0;
+#pragma unroll 8
+    for (int m = 0; m < n; ++m) {
+      const int km = key[m];
+      r += (km > kj) | ((km == kj) & (m < tid));
+    }
+    if (r == k) {  // ranks are a permutation of 0 .. n - 1: exactly one thread
+      pick[0] = tid;
+      pick[1] = sj;
+      pick[2] = kj;
+    }
+  }
+  lds_barrier();
+  i = pick[0];
+  s_out = pick[1];
+  L_out = pick[2];
 }
 
 // Load the block ids of logical pages [lp0, lp0 + npages) into LDS and
@@ -630,7 +691,10 @@ struct KVTile {
   u32x4_t v[DH / 16];   // V^T: 16 dims x 8 tokens per lane
 };
 
-template <int DH, bool STEP>
+// ORD: the grid takes the (request, kv head) pairs in length order (see
+// order_pick); a separate instantiation, so that the grid-order kernels
+// carry none of its code.
+template <int DH, bool STEP, bool ORD>
 __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a) {
   __shared__ int pages[kMaxChunkPages];
   __shared__ int flag;
@@ -642,10 +706,14 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
   __shared__ int step_bad_page[kDecWaves];
   __shared__ int step_plan_sh[2];     // ... the append commits; block popped for this request
 
-  const int c = blockIdx.x, g = blockIdx.y, i = blockIdx.z;
+  const int c = blockIdx.x;
+  int g = blockIdx.y, i = blockIdx.z;  // (request, kv head): grid position, or by length order
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int bs_log2 = a.bs_log2, bs = 1 << bs_log2;
   int s = 0, L = 0, st = 0, L_pool = 0;  // chunking covers [0, L), the pool holds [0, L_pool)
+  const bool ordered = ORD && i < a.order_n;  // (the step's commit row is not)
+  int s_ord = 0, L_ord = 0;
+  __shared__ int ord_key[ORD ? kDecThreads : 1], ord_pick[3];
   int nc = 0, chunk = 0, t0 = 0, t1 = 0, lp0 = 0, npages = 0;
   bool work = false, pages_ok = true;
 
@@ -670,11 +738,13 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     // this request's id, length and page ids; the plan itself is worked
     // out after the streaming loop, where it is first needed
     if (w == kDecWaves - 1) step_plan_read1(a, pr);
-    s = a.seq_ids[i];
+    if constexpr (ORD)
+      if (ordered) order_pick(a, g, i, s_ord, L_ord, ord_key, ord_pick);
+    s = ordered ? s_ord : a.seq_ids[i];
     const int frozen = *a.err != 0;
     const bool own_ok = s >= 0 && s < a.max_seqs;
     if (w == kDecWaves - 1) step_plan_read2(a, pr);
-    L_pool = own_ok ? a.lengths[s] : 0;
+    L_pool = own_ok ? (ordered ? L_ord : a.lengths[s]) : 0;
     if (!own_ok || L_pool < 0 || L_pool > (a.max_blocks << bs_log2)) st = SM_ERR_EINVAL;
     own_can = !frozen && st == 0 && (int64_t)L_pool + 1 <= a.cap;
     if (st == 0) {  // chunked for the appended length whenever this request can append
@@ -734,8 +804,10 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
 #pragma unroll
     for (int ww = 0; ww < kDecWaves; ++ww) pages_ok = pages_ok && !step_bad_page[ww];
   } else {
-    s = a.seq_ids[i];
-    st = seq_status(a, s, L);
+    if constexpr (ORD)
+      if (ordered) order_pick(a, g, i, s_ord, L_ord, ord_key, ord_pick);
+    s = ordered ? s_ord : a.seq_ids[i];
+    st = seq_status(a, s, L, ordered, L_ord);
     L_pool = L;
     work = st == 0 && L > 0;
     if (work) {
@@ -1308,18 +1380,61 @@ static sm_status decode_setup(const sm_paged_cache *c, const int32_t *seq_ids, i
   return SM_OK;
 }
 
+// Compute units of the current device (looked up once per device), or 0.
+static int device_cus() {
+  static std::atomic<int> cus[64];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  int v = cus[dev].load(std::memory_order_relaxed);
+  if (v <= 0) {
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) return 0;
+    cus[dev].store(v, std::memory_order_relaxed);
+  }
+  return v;
+}
+
+// Workgroups of a bf16 decode kernel resident on one compute unit at once.
+template <int DH, bool STEP>
+static int bf16_occupancy() {
+  static const int occ = [] {
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_split_bf16<DH, STEP, true>, kDecThreads, 0) !=
+        hipSuccess)
+      nb = 1;
+    return nb > 0 ? nb : 1;
+  }();
+  return occ;
+}
+
 template <bool STEP>
-static sm_status decode_launch(const sm_paged_cache *c, const DecodeArgs &a, int n, hipStream_t stream) {
+static sm_status decode_launch(const sm_paged_cache *c, DecodeArgs a, int n, hipStream_t stream) {
   // one launch: split, and the last workgroup of each (sequence, kv head)
   // combines; with max_len = 0 the single chunk column writes zero rows
   // a fused bf16 step adds one grid row: its first workgroup commits the append
   const int rows = n + ((STEP && c->dtype == SM_BF16) ? 1 : 0);
   const dim3 grid(a.max_chunks, c->num_kv_heads, rows);
+  if (c->dtype == SM_BF16 && a.max_chunks == 1 && n <= kDecThreads) {
+    // more single-chunk pairs than compute units: deal them longest first
+    const int cus = device_cus();
+    if (cus > 0 && (int64_t)n * c->num_kv_heads > cus) {
+      a.order_n = n;
+      a.order_cus = cus;
+      a.order_occ = c->head_dim == 128 ? bf16_occupancy<128, STEP>() : bf16_occupancy<64, STEP>();
+    }
+  }
   if (c->dtype == SM_BF16) {
-    if (c->head_dim == 128)
-      hipLaunchKernelGGL((decode_split_bf16<128, STEP>), grid, dim3(kDecThreads), 0, stream, a);
-    else
-      hipLaunchKernelGGL((decode_split_bf16<64, STEP>), grid, dim3(kDecThreads), 0, stream, a);
+    const bool ord = a.order_n > 0;
+    if (c->head_dim == 128) {
+      if (ord)
+        hipLaunchKernelGGL((decode_split_bf16<128, STEP, true>), grid, dim3(kDecThreads), 0, stream, a);
+      else
+        hipLaunchKernelGGL((decode_split_bf16<128, STEP, false>), grid, dim3(kDecThreads), 0, stream, a);
+    } else {
+      if (ord)
+        hipLaunchKernelGGL((decode_split_bf16<64, STEP, true>), grid, dim3(kDecThreads), 0, stream, a);
+      else
+        hipLaunchKernelGGL((decode_split_bf16<64, STEP, false>), grid, dim3(kDecThreads), 0, stream, a);
+    }
   } else {
     if (c->head_dim == 128)
       hipLaunchKernelGGL((decode_split_f32<128, STEP>), grid, dim3(kDecThreads), 0, stream, a);

@@ -113,3 +113,67 @@ def test_decode_error_rows_are_zero(orc):
     assert st == orc.EINVAL
     assert c.error_bits() == sm.ERR_EINVAL
     assert torch.all(out[1] == 0)
+
+
+def _ragged(rng, n, hi):
+    """n cached lengths: the page edges 0, 1, 15, 16, 17, 31, 32, 33 and
+    hi, the rest uniform in [0, hi]."""
+    edges = [0, 1, 15, 16, 17, 31, 32, 33, hi]
+    lens = list(rng.randint(0, hi + 1, size=n))
+    lens[:len(edges)] = edges[:n]
+    rng.shuffle(lens)
+    return [int(x) for x in lens]
+
+
+# More single-chunk (sequence, kv head) pairs than compute units: each
+# workgroup takes its pair from the requests sorted by cached length
+# (longest first), the first resident rounds dealt in alternating order.
+# Cases: a partial second round (280 and 400 pairs), exactly two rounds
+# (512), and more pairs than resident workgroups (2048: the rest are
+# dispatched as compute units free up).
+ORDERED = [
+    # Hq, H, D, n, longest length
+    (28, 4, 128, 70, 1500),
+    (28, 4, 128, 100, 4096),
+    (32, 8, 64, 64, 700),
+    (32, 8, 64, 256, 400),
+]
+
+
+@pytest.mark.parametrize("case", range(len(ORDERED)))
+def test_decode_pairs_dealt_by_length(orc, case):
+    Hq, H, D, n, hi = ORDERED[case]
+    rng = np.random.RandomState(300 + case)
+    lens = _ragged(rng, n, hi)
+    say("decode dealt by length: Hq", Hq, "H", H, "D", D, "n", n, "pairs", n * H, "longest", hi)
+    oc, c = _setup(orc, rng, torch.bfloat16, Hq, H, D, 16, lens)
+    ids = rng.permutation(n)
+    st, ref, out = _run(orc, oc, c, torch.bfloat16, Hq, ids, hi + 5, rng)
+    assert st == orc.OK and c.error_bits() == 0
+    err = rel_l2_max(out.float().numpy(), ref)
+    say("rel_l2_max", err)
+    assert err <= TOL[torch.bfloat16]
+    # requests that attend over nothing get zero rows
+    for j, s in enumerate(ids):
+        if lens[s] == 0:
+            assert torch.all(out[j] == 0)
+
+
+def test_decode_pairs_dealt_by_length_with_bad_ids(orc):
+    """Ids out of range sort last (key -1) and get zero rows and EINVAL; a
+    repeated id takes two ranks."""
+    rng = np.random.RandomState(41)
+    n, H, Hq, D = 90, 4, 28, 128
+    lens = _ragged(rng, n, 900)
+    oc, c = _setup(orc, rng, torch.bfloat16, Hq, H, D, 16, lens)
+    ids = rng.permutation(n).astype(np.int64)
+    ids[3] = oc.max_seqs + 7
+    ids[50] = -1
+    ids[60] = ids[61]
+    say("decode dealt by length, bad ids at 3 and 50, repeated id at 60/61")
+    st, ref, out = _run(orc, oc, c, torch.bfloat16, Hq, ids, 905, rng)
+    assert st == orc.EINVAL
+    assert c.error_bits() == sm.ERR_EINVAL
+    assert torch.all(out[3] == 0) and torch.all(out[50] == 0)
+    good = [j for j in range(n) if j not in (3, 50)]
+    assert rel_l2_max(out[good].float().numpy(), ref[good]) <= TOL[torch.bfloat16]

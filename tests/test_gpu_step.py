@@ -379,3 +379,31 @@ def test_commit_wait_give_up_commits_nothing_and_reports_einval(orc):
     e = rel_l2_max(out.float().numpy(), ref)
     say("step after the give-up: rel_l2_max", e)
     assert e <= TOL[dtype]
+
+
+@pytest.mark.parametrize("n,H,Hq,D,hi", [(100, 4, 28, 128, 3000), (128, 4, 28, 128, 300), (200, 8, 32, 64, 90)])
+def test_step_pairs_dealt_by_length(orc, n, H, Hq, D, hi):
+    """More single-chunk (sequence, kv head) pairs than compute units: the
+    workgroups take the pairs longest first.  Lengths include 0, 1 and the
+    page edges, so some requests pop a block; two steps in a row."""
+    dtype, bs = torch.bfloat16, 16
+    rng = np.random.RandomState(2000 + n)
+    edges = [0, 1, 15, 16, 17, 31, 32, 33, hi]
+    lens = list(rng.randint(0, hi + 1, size=n))
+    lens[:len(edges)] = edges
+    rng.shuffle(lens)
+    oc, c = _cache(orc, rng, dtype, H, D, bs, lens, MB=-(-(hi + 2) // bs) + 2)
+    ids = rng.permutation(n)
+    ws = None
+    for step in range(2):
+        K, V, q = _inputs(rng, dtype, n, H, Hq, D)
+        st_a, st_d, ref = _oracle_step(orc, oc, ids, K, V, q, Hq)
+        assert st_a == orc.OK
+        say("decode step dealt by length: n", n, "H", H, "pairs", n * H, "step", step)
+        out, ws = _gpu_step(c, ids, K, V, q, hi + 2, ws)
+        assert c.error_bits() == 0
+        assert_same_state(c, oc)
+        _counters_clear(ws)
+        err = rel_l2_max(out.float().numpy(), ref)
+        say("rel_l2_max", err)
+        assert err <= TOL[dtype]
