@@ -227,30 +227,34 @@ class Job:
     def _merge(self, rs, s, lane, st):
         """Decode-time merge of batches rs (at most merge_group of them, all
         on `lane`) before decode step s: the merge module on every
-        sequence's freshly completed span, in one call, and each batch's roll
-        back of n-1 entries per sequence (the surrogate's K/V is then the
-        step's appended row)."""
-        L, w = self.L, self.w
+        sequence's freshly completed span, in one call.  The crop of the
+        span's n-1 cached entries happens in the step's own launch."""
+        w = self.w
         B = w.batch
         m = self.dmerge[s]
         S = len(rs) * B
         rc = self._merge_call(m["g_row_idx"].data_ptr(), len(rs) * m["rows"], m["g_offs"].data_ptr(), S,
                               self.zdec[lane].data_ptr(), self.dmerge_ws[lane], st)
-        for r in rs:
-            rc |= L.sm_kv_rollback(self.descs[r], self.ids.data_ptr(), m["k"].data_ptr(), B, st)
         if rc:
             raise RuntimeError(f"decode-time merge launch failed at step {s}: {rc}")
 
     def _step(self, r, s, st):
-        """Decode step s of batch r: append the step's K/V row (new token or
-        surrogate) and attend, in one launch."""
+        """Decode step s of batch r in one launch: append the step's K/V row
+        (new token, or at a merge step the surrogate's after cropping the
+        span's n-1 entries) and attend."""
         L, w = self.L, self.w
         j = s % self.nin
         lane = r % self.lanes
         ws = self.dec_ws[lane]
-        rc = L.sm_decode_step(self.descs[r], self.ids.data_ptr(), w.batch, self.Kt[j].data_ptr(),
-                              self.Vt[j].data_ptr(), self.q[j].data_ptr(), w.num_q_heads, w.head_dim ** -0.5,
-                              self.max_len, self.out[lane].data_ptr(), ws.data_ptr(), ws.numel(), st)
+        if s in self.dmerge:
+            rc = L.sm_decode_merge_step(self.descs[r], self.ids.data_ptr(), self.dmerge[s]["k"].data_ptr(), w.batch,
+                                        self.Kt[j].data_ptr(), self.Vt[j].data_ptr(), self.q[j].data_ptr(),
+                                        w.num_q_heads, w.head_dim ** -0.5, self.max_len,
+                                        self.out[lane].data_ptr(), ws.data_ptr(), ws.numel(), st)
+        else:
+            rc = L.sm_decode_step(self.descs[r], self.ids.data_ptr(), w.batch, self.Kt[j].data_ptr(),
+                                  self.Vt[j].data_ptr(), self.q[j].data_ptr(), w.num_q_heads, w.head_dim ** -0.5,
+                                  self.max_len, self.out[lane].data_ptr(), ws.data_ptr(), ws.numel(), st)
         if rc:
             raise RuntimeError(f"decode step launch failed at step {s}: {rc}")
 
@@ -696,17 +700,19 @@ def config_decode_report(cid, dev, stream, reps=3, merge_every=None):
 
     def loop(ev=None):
         for s_ in range(S):
-            if s_ in kdev:
-                for d in descs:
-                    L.sm_kv_rollback(d, ids.data_ptr(), kdev[s_].data_ptr(), B, st)
             j = s_ % nin
             if ev is not None:
                 ev[0][s_].record(stream)
             for d in descs:
-                rc = L.sm_decode_step(d, ids.data_ptr(), B, Kt[j].data_ptr(), Vt[j].data_ptr(), q[j].data_ptr(), Hq,
-                                      scale, max_len, out.data_ptr(), ws.data_ptr(), ws.numel(), st)
+                if s_ in kdev:  # crop the span's n - 1 entries, append the surrogate's row, attend
+                    rc = L.sm_decode_merge_step(d, ids.data_ptr(), kdev[s_].data_ptr(), B, Kt[j].data_ptr(),
+                                                Vt[j].data_ptr(), q[j].data_ptr(), Hq, scale, max_len,
+                                                out.data_ptr(), ws.data_ptr(), ws.numel(), st)
+                else:
+                    rc = L.sm_decode_step(d, ids.data_ptr(), B, Kt[j].data_ptr(), Vt[j].data_ptr(), q[j].data_ptr(),
+                                          Hq, scale, max_len, out.data_ptr(), ws.data_ptr(), ws.numel(), st)
                 if rc:
-                    raise RuntimeError(f"sm_decode_step failed at config {cid} step {s_}: {rc}")
+                    raise RuntimeError(f"decode step failed at config {cid} step {s_}: {rc}")
             if ev is not None:
                 ev[1][s_].record(stream)
 
@@ -717,7 +723,7 @@ def config_decode_report(cid, dev, stream, reps=3, merge_every=None):
     loop()
     undo()
     torch.cuda.synchronize()
-    elapsed, kern = [], []
+    elapsed, kern, per_merge, per_plain = [], [], [], []
     for _ in range(reps):
         ev = [[torch.cuda.Event(enable_timing=True) for _ in range(S)] for _ in range(2)]
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -727,7 +733,10 @@ def config_decode_report(cid, dev, stream, reps=3, merge_every=None):
         undo()
         torch.cuda.synchronize()
         elapsed.append(e0.elapsed_time(e1))
-        kern.append(sum(a.elapsed_time(b) for a, b in zip(ev[0], ev[1])))
+        per = [a.elapsed_time(b) for a, b in zip(ev[0], ev[1])]
+        kern.append(sum(per))
+        per_merge.append(sum(per[x] for x in kdev) / max(1, len(kdev)))
+        per_plain.append(sum(per[x] for x in range(S) if x not in kdev) / max(1, S - len(kdev)))
     bad = [c.error_bits() for c in caches]
     if any(bad):
         raise RuntimeError(f"config {cid}: device error bits {bad}")
@@ -745,9 +754,11 @@ def config_decode_report(cid, dev, stream, reps=3, merge_every=None):
         "avg_launch_us": round(launch_us, 3),
         "algorithmic_MB_per_launch": round(sum(step_bytes) / S / 1e6, 2),
         "achieved_GBps": round(gbps, 1), "frac": round(gbps / PEAK_HBM_GBS, 4),
-        "note": "one stream; tokens/s = B x steps x replicas over the loop's time (best of %d), including the "
-                "rollback launches of the merge steps; launch time from HIP events around each step's "
-                "back-to-back launches" % reps}
+        "merge_step_launch_us": round(min(per_merge) * 1e3 / R, 3) if kdev else None,
+        "plain_step_launch_us": round(min(per_plain) * 1e3 / R, 3),
+        "note": "one stream; tokens/s = B x steps x replicas over the loop's time (best of %d); a merge step is "
+                "one sm_decode_merge_step launch per replica (crop n-1, append, attend), the others "
+                "sm_decode_step; launch time from HIP events around each step's back-to-back launches" % reps}
     del caches, ws
     torch.cuda.empty_cache()
     log(f"config {cid}: {res['avg_launch_us']} us per launch, {res['achieved_GBps']} GB/s")

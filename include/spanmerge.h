@@ -369,6 +369,43 @@ sm_status sm_decode_step(const sm_paged_cache *c, const int32_t *seq_ids,
                          void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * sm_decode_merge_step -- the decode step at which spans complete, in one
+ * launch ("Decoding-Time Merging and KV-Cache Update"; "Decoding-time
+ * Integration"): each request first drops its last crop[i] cached entries
+ * (the raw tokens of the span that just completed, n - 1 of them), then its
+ * row (the surrogate's K/V state, or the plain token's when crop[i] = 0) is
+ * appended, and its query attends over the result: the cache goes from L to
+ * L - crop[i] + 1 entries.  The crops and the append are one update, made
+ * whole or not at all: its state and error bits are those of
+ *   sm_kv_rollback(c, seq_ids, crop, n)
+ *   sm_kv_append(c, seq_ids, {0, 1, ..., n}, n, n, K, V)
+ * issued back to back when both succeed (the freed pages go onto the free
+ * stack and the append pops from it exactly as the two calls do); when
+ * either would fail, the cache is left as it was, the error bits of the
+ * first failing check are set, and the attention runs over the unchanged
+ * cache (as sm_decode_step's does when its append fails).  A rule match
+ * decides the crops: sm_match_decode with cache = NULL writes them to k_out
+ * without cropping, ready to pass here.
+ *
+ *  c            bf16 caches only (SM_EINVAL otherwise)
+ *  seq_ids      [n] distinct ids, n <= 256
+ *  crop         [n] (device) entries to drop per request, 0 <= crop[i] <=
+ *               lengths[seq_ids[i]]
+ *  K, V, q, num_q_heads, scale, out, ws, ws_bytes: as sm_decode_step
+ *  max_len      (host) upper bound on the lengths before the crops
+ * Device errors: EINVAL (bad or repeated id, negative crop, corrupt free
+ * stack or block table), ERANGE (crop longer than the cache, no room on the
+ * free stack for the freed blocks, length above capacity after the append),
+ * ENOMEM (no free block for the append), then those of
+ * sm_decode_attention.
+ */
+sm_status sm_decode_merge_step(const sm_paged_cache *c, const int32_t *seq_ids,
+                               const int32_t *crop, int n, const void *K,
+                               const void *V, const void *q, int num_q_heads,
+                               float scale, int max_len, void *out, void *ws,
+                               size_t ws_bytes, hipStream_t stream);
+
+/*
  * sm_set_commit_wait_limit -- for tests of a fused step's give-up path (not
  * for production use).  A fused step's append is committed by one extra
  * workgroup once every attention workgroup has read the metadata; it polls

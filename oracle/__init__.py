@@ -309,6 +309,25 @@ class OracleCache:
         return lib().orc_kv_append(C.byref(s), _ptr(seq_ids), _ptr(row_offsets),
                                    seq_ids.shape[0], _ptr(K), _ptr(V))
 
+    def crop_append(self, seq_ids, k, K, V):
+        """The decode-time merge update of the cache ("Decoding-Time Merging
+        and KV-Cache Update"): request i drops its last k[i] entries, then
+        its one row K[i], V[i] is appended (L -> L - k + 1).  The two steps
+        are rollback() and append() as they stand, taken as one update: if
+        either fails, every array is put back as it was and that step's
+        status is returned."""
+        saved = [a.copy() for a in (self.lengths, self.block_table, self.free_stack, self.free_top,
+                                    self.k_pool, self.v_pool)]
+        n = len(seq_ids)
+        st = self.rollback(seq_ids, k)
+        if st == OK:
+            st = self.append(seq_ids, np.arange(n + 1, dtype=np.int32), K, V)
+        if st != OK:
+            for a, b in zip((self.lengths, self.block_table, self.free_stack, self.free_top,
+                             self.k_pool, self.v_pool), saved):
+                a[...] = b
+        return st
+
     def decode_attention(self, seq_ids, q, num_q_heads, scale, return_probs=False):
         seq_ids = _i32(seq_ids)
         q = _f64(q)

@@ -73,6 +73,9 @@ struct DecodeArgs {
   // grid's workgroups take the (sequence, head) pairs longest first, dealt
   // over order_cus compute units holding order_occ workgroups each
   int order_n, order_cus, order_occ;
+  // decode-time merge step only (sm_decode_merge_step): entries cropped
+  // from each request's cache before its row is appended, request order
+  const int32_t *crop;
 };
 
 // Chunking of a sequence of L cached entries: nc non-empty chunks of
@@ -413,9 +416,11 @@ __device__ bool step_pages(const DecodeArgs &a, StepShared &sp, int incl, int ne
 // stack (the blocks the call may pop).
 struct PlanRegs {
   int sk[4], Lk[4], win[4];
+  int ck[4];  // entries cropped first (decode-time merge step; else unused)
   int frozen, top;
 };
 
+template <bool CROP = false>
 __device__ __forceinline__ void step_plan_read1(const DecodeArgs &a, PlanRegs &pr) {
   const int lane = threadIdx.x & 63;
   pr.frozen = *a.err != 0;
@@ -424,6 +429,7 @@ __device__ __forceinline__ void step_plan_read1(const DecodeArgs &a, PlanRegs &p
   for (int k = 0; k < 4; ++k) {
     const int t = lane + 64 * k;
     pr.sk[k] = t < a.n ? a.seq_ids[t] : -1;
+    if constexpr (CROP) pr.ck[k] = t < a.n ? a.crop[t] : 0;
   }
 }
 
@@ -450,28 +456,56 @@ struct PlanOut {
   int pop[4];   // ... and which one (or -1)
 };
 
-__device__ void plan_regs(const DecodeArgs &a, const PlanRegs &pr, PlanOut &po) {
+// Whether any id occurs twice among the n requests (lane l of the calling
+// wave holds requests l + 64 k).  With the bitmap (one bit per sequence id,
+// max_seqs <= 32 * kDupBitmapWords) it takes one LDS atomic per request;
+// otherwise every earlier id is compared, a loop of n steps.  Only the
+// calling wave uses the bitmap, and its LDS operations complete in order,
+// so the clearing stores precede the atomics.
+constexpr int kDupBitmapWords = 1024;
+
+__device__ bool wave_any_dup(const DecodeArgs &a, const int (&sk)[4], uint32_t *bm) {
   const int lane = threadIdx.x & 63, n = a.n;
-  int dup[4] = {0, 0, 0, 0};
+  int dup = 0;
+  if (bm && a.max_seqs <= 32 * kDupBitmapWords) {
+    const int words = (a.max_seqs + 31) >> 5;
+    for (int wd = lane; wd < words; wd += kWave) bm[wd] = 0u;
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {  // every earlier request, 64 at a time
-    if (64 * kk < n) {
-      const int jn = min(64, n - 64 * kk);
-      for (int jl = 0; jl < jn; ++jl) {
-        const int idj = __builtin_amdgcn_readlane(pr.sk[kk], jl);
-        const int j = 64 * kk + jl;
+    for (int k = 0; k < 4; ++k) {
+      const int t = lane + 64 * k, s = sk[k];
+      if (t < n && s >= 0 && s < a.max_seqs) {
+        const uint32_t bit = 1u << (s & 31);
+        const uint32_t old = __hip_atomic_fetch_or(&bm[s >> 5], bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        dup |= (old & bit) != 0;
+      }
+    }
+  } else {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) dup[k] |= (j < lane + 64 * k) && idj == pr.sk[k];
+    for (int kk = 0; kk < 4; ++kk) {  // every earlier request, 64 at a time
+      if (64 * kk < n) {
+        const int jn = min(64, n - 64 * kk);
+        for (int jl = 0; jl < jn; ++jl) {
+          const int idj = __builtin_amdgcn_readlane(sk[kk], jl);
+          const int j = 64 * kk + jl;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) dup |= (j < lane + 64 * k) && (lane + 64 * k < n) && idj == sk[k];
+        }
       }
     }
   }
+  return __ballot(dup) != 0;
+}
+
+__device__ void plan_regs(const DecodeArgs &a, const PlanRegs &pr, PlanOut &po, uint32_t *bm) {
+  const int lane = threadIdx.x & 63, n = a.n;
+  const bool any_dup = wave_any_dup(a, pr.sk, bm);
   int inval = 0, range = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int t = lane + 64 * k, sk = pr.sk[k], Lk = pr.Lk[k];
     po.need[k] = 0;
     if (t < n) {
-      if (sk < 0 || sk >= a.max_seqs || dup[k]) inval = 1;
+      if (sk < 0 || sk >= a.max_seqs || any_dup) inval = 1;
       else if (Lk < 0 || (int64_t)Lk + 1 > a.cap) range = 1;
       else po.need[k] = (Lk & ((1 << a.bs_log2) - 1)) == 0;
     }
@@ -561,9 +595,9 @@ __device__ void plan_regs_one(const DecodeArgs &a, const PlanRegs &pr, PlanOut &
   po.total = total;
 }
 
-__device__ __forceinline__ void plan_any(const DecodeArgs &a, const PlanRegs &pr, PlanOut &po) {
+__device__ __forceinline__ void plan_any(const DecodeArgs &a, const PlanRegs &pr, PlanOut &po, uint32_t *bm) {
   if (a.n <= 64) plan_regs_one(a, pr, po);
-  else plan_regs(a, pr, po);
+  else plan_regs(a, pr, po, bm);
 }
 
 // Value of request i's slot k-array entry (held by lane i % 64) in every lane.
@@ -586,13 +620,13 @@ __device__ __forceinline__ int request_value(const int (&v)[4], int i) {
 // its next call.  (A lower bound can be set for tests of this path.)
 constexpr int kCommitSpinLimit = 1 << 20;
 
-__device__ void step_commit_wave(const DecodeArgs &a) {
+__device__ void step_commit_wave(const DecodeArgs &a, uint32_t *bm) {
   const int lane = threadIdx.x & 63;
   PlanRegs pr;
   step_plan_read1(a, pr);
   step_plan_read2(a, pr);
   PlanOut po;
-  plan_any(a, pr, po);
+  plan_any(a, pr, po, bm);
   int arrived = 0;
   if (lane == 0) {
     for (int it = 0; it < a.spin_limit; ++it) {
@@ -617,6 +651,229 @@ __device__ void step_commit_wave(const DecodeArgs &a) {
   }
   if (lane == 0) {
     if (arrived && po.ok) *a.free_top = pr.top - po.total;
+    int bits = __hip_atomic_load(a.step_err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) | po.bits;
+    if (!arrived) bits |= SM_ERR_EINVAL;  // not reached while every workgroup arrives
+    if (bits) set_err(a.err, bits);
+    __hip_atomic_store(a.step_err, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(a.step_arrivals, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// The plan of a decode-time merge step (one wave, registers only, lane l
+// holding requests l + 64 k): crop c_t entries of request t, then append
+// its one row, as one update that is made whole or not at all.  The checks
+// come in the order of the two operations: ids (in range, no repeats) and
+// c_t >= 0, else EINVAL; 0 <= L_t <= capacity and c_t <= L_t, then room on
+// the free stack for every freed block, then L_t - c_t + 1 <= capacity,
+// else ERANGE; enough free blocks after the crop, else ENOMEM; every block
+// popped a valid id, else EINVAL.  The crop pushes request t's freed pages
+// (pages of entries >= L_t - c_t) onto the free stack, highest page first,
+// requests in reverse order; the append then pops, requests in order, one
+// block for each request whose cropped length ends a page.  So the c-th
+// pop takes, while c <= F (the blocks all crops free), the c-th freed page
+// in the order (request 0's pages ascending, then request 1's, ...), and
+// after that the old stack's entry top - 1 - (c - F - 1).
+struct PlanOutC {
+  bool ok;      // the update commits
+  int bits;     // its error bits (0 when the error word was set)
+  int total;    // blocks popped
+  int freed;    // blocks pushed by the crops
+  int need[4];  // per request of this lane: a block is popped for it
+  int pop[4];   // ... and which one (or -1)
+  int F[4];     // blocks its crop frees
+  int E[4];     // blocks freed by the requests before it
+  int Lc[4];    // its length after the crop
+};
+
+__device__ __forceinline__ int blocks_for_len(int L, int bs_log2) { return (L + (1 << bs_log2) - 1) >> bs_log2; }
+
+// Inclusive prefix sum over the wave's lanes.
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int u = __shfl_up(v, d, kWave);
+    if (lane >= d) v += u;
+  }
+  return v;
+}
+
+__device__ void plan_crop(const DecodeArgs &a, const PlanRegs &pr, PlanOutC &po, uint32_t *bm) {
+  const int lane = threadIdx.x & 63, n = a.n, bsl = a.bs_log2;
+  const bool any_dup = wave_any_dup(a, pr.sk, bm);
+  int inval = 0, range = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int t = lane + 64 * k, sk = pr.sk[k], Lk = pr.Lk[k], ck = pr.ck[k];
+    po.need[k] = 0;
+    po.F[k] = 0;
+    po.Lc[k] = 0;
+    if (t < n) {
+      if (sk < 0 || sk >= a.max_seqs || any_dup || ck < 0) inval = 1;
+      else if (Lk < 0 || (int64_t)Lk > a.cap || ck > Lk) range = 1;
+      else {
+        const int Lc = Lk - ck;
+        po.Lc[k] = Lc;
+        po.F[k] = blocks_for_len(Lk, bsl) - blocks_for_len(Lc, bsl);
+        if ((int64_t)Lc + 1 > a.cap) range = 1;
+        po.need[k] = (Lc & ((1 << bsl) - 1)) == 0;
+      }
+    }
+  }
+  const bool any_inval = __ballot(inval) != 0;
+  const bool any_range = __ballot(range) != 0;
+  int incl[4] = {0, 0, 0, 0}, total = 0, freed = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {  // prefixes in request order
+    if (64 * k < n) {
+      const uint64_t m = __ballot(po.need[k]);
+      const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+      incl[k] = total + below + po.need[k];
+      total += __popcll(m);
+      const int f_incl = wave_incl_scan(po.F[k]);
+      po.E[k] = freed + f_incl - po.F[k];
+      freed += __shfl(f_incl, 63, kWave);
+    } else {
+      po.E[k] = freed;
+    }
+  }
+  const int top = pr.top;
+  int bits = any_inval ? SM_ERR_EINVAL
+             : (any_range || top < 0 || (int64_t)top + freed > a.num_blocks) ? SM_ERR_ERANGE
+             : (total > top + freed) ? SM_ERR_ENOMEM
+                                     : 0;
+  const bool go = !pr.frozen && bits == 0;
+  // pops of freed pages: the owner of the c-th freed page, looked up over
+  // the requests whose crop frees any
+  int own_s[4] = {-1, -1, -1, -1}, own_pg[4] = {0, 0, 0, 0};
+  if (go && freed > 0) {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      if (64 * kk < n) {
+        uint64_t m = __ballot(po.F[kk] > 0);
+        while (m) {
+          const int jl = __builtin_ctzll(m);
+          m &= m - 1;
+          const int Ej = __builtin_amdgcn_readlane(po.E[kk], jl), Fj = __builtin_amdgcn_readlane(po.F[kk], jl);
+          const int sj = __builtin_amdgcn_readlane(pr.sk[kk], jl), Lcj = __builtin_amdgcn_readlane(po.Lc[kk], jl);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const int cidx = incl[k];
+            if (po.need[k] && cidx > Ej && cidx <= Ej + Fj) {
+              own_s[k] = sj;
+              own_pg[k] = blocks_for_len(Lcj, bsl) + (cidx - Ej - 1);
+            }
+          }
+        }
+      }
+    }
+  }
+  int bad = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    po.pop[k] = -1;
+    if (64 * k < n) {
+      const bool popped = go && po.need[k];
+      // from the old stack: entry incl - freed - 1 < total - freed <= min(top, n) of the window
+      const int widx = (popped && incl[k] > freed) ? incl[k] - freed - 1 : 0;
+      int blk = __shfl(pr.win[0], widx & 63, kWave);
+      if (total > 64) {
+        const int w1 = __shfl(pr.win[1], widx & 63, kWave);
+        const int w2 = __shfl(pr.win[2], widx & 63, kWave), w3 = __shfl(pr.win[3], widx & 63, kWave);
+        const int q = widx >> 6;
+        blk = q == 0 ? blk : q == 1 ? w1 : q == 2 ? w2 : w3;
+      }
+      if (popped && incl[k] <= freed)
+        blk = own_s[k] >= 0 ? a.block_table[(int64_t)own_s[k] * a.max_blocks + own_pg[k]] : -1;
+      po.pop[k] = popped ? blk : -1;
+      if (popped && (blk < 0 || blk >= a.num_blocks)) bad = 1;
+    }
+  }
+  const bool any_stack = __ballot(bad) != 0;
+  if (go && any_stack) bits = SM_ERR_EINVAL;  // corrupt free stack or block table
+  po.ok = go && !any_stack;
+  po.bits = pr.frozen ? 0 : bits;
+  po.total = total;
+  po.freed = freed;
+}
+
+// The commit wave of a decode-time merge step: as step_commit_wave, and
+// the crops' writes before the append's: the freed pages' block ids go onto
+// the free stack (request t's at top + freed - E_t - F_t onward, highest
+// page first) and their table entries become -1; then each popped block
+// enters its request's table, lengths become L_t - c_t + 1 and the stack top
+// top + freed - popped.
+__device__ void step_commit_wave_crop(const DecodeArgs &a, uint32_t *bm) {
+  const int lane = threadIdx.x & 63, bsl = a.bs_log2;
+  PlanRegs pr;
+  step_plan_read1<true>(a, pr);
+  step_plan_read2(a, pr);
+  PlanOutC po;
+  plan_crop(a, pr, po, bm);
+  int arrived = 0;
+  if (lane == 0) {
+    for (int it = 0; it < a.spin_limit; ++it) {
+      if (__hip_atomic_load(a.step_arrivals, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= a.total_wgs) {
+        arrived = 1;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(8);
+    }
+  }
+  arrived = __shfl(arrived, 0, kWave);
+  if (arrived && po.ok) {
+    // push slot p of [0, freed) (stack entry top + p) holds the c-th freed
+    // page in pop order, c = freed - p; a lane takes four slots at a time:
+    // owners found, the table entries read, then the stack written and the
+    // entries cleared (all reads before any write)
+    for (int p0 = 0; p0 < po.freed; p0 += 4 * kWave) {
+      int own_s[4] = {-1, -1, -1, -1}, own_pg[4] = {0, 0, 0, 0};
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        if (64 * kk < a.n) {
+          uint64_t m = __ballot(po.F[kk] > 0);
+          while (m) {
+            const int jl = __builtin_ctzll(m);
+            m &= m - 1;
+            const int Ej = __builtin_amdgcn_readlane(po.E[kk], jl), Fj = __builtin_amdgcn_readlane(po.F[kk], jl);
+            const int sj = __builtin_amdgcn_readlane(pr.sk[kk], jl), Lcj = __builtin_amdgcn_readlane(po.Lc[kk], jl);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int cidx = po.freed - (p0 + lane + kWave * r);
+              if (cidx > Ej && cidx <= Ej + Fj) {
+                own_s[r] = sj;
+                own_pg[r] = blocks_for_len(Lcj, bsl) + (cidx - Ej - 1);
+              }
+            }
+          }
+        }
+      }
+      int blk[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        blk[r] = own_s[r] >= 0 ? a.block_table_w[(int64_t)own_s[r] * a.max_blocks + own_pg[r]] : -1;
+      __builtin_amdgcn_s_waitcnt(0);  // every read of the table before its entries are cleared
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (own_s[r] >= 0) {
+          a.free_stack[pr.top + p0 + lane + kWave * r] = blk[r];
+          a.block_table_w[(int64_t)own_s[r] * a.max_blocks + own_pg[r]] = -1;
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0);  // cleared before the pops are written (a pop may land on one)
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int t = lane + 64 * k;
+      if (t < a.n) {
+        const int s = pr.sk[k], Lc = po.Lc[k];
+        if (po.pop[k] >= 0) a.block_table_w[(int64_t)s * a.max_blocks + (Lc >> bsl)] = po.pop[k];
+        a.lengths_w[s] = Lc + 1;
+      }
+    }
+  }
+  if (lane == 0) {
+    if (arrived && po.ok) *a.free_top = pr.top + po.freed - po.total;
     int bits = __hip_atomic_load(a.step_err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) | po.bits;
     if (!arrived) bits |= SM_ERR_EINVAL;  // not reached while every workgroup arrives
     if (bits) set_err(a.err, bits);
@@ -694,7 +951,9 @@ struct KVTile {
 // ORD: the grid takes the (request, kv head) pairs in length order (see
 // order_pick); a separate instantiation, so that the grid-order kernels
 // carry none of its code.
-template <int DH, bool STEP, bool ORD>
+// CROP (with STEP): the decode-time merge step; the crops and the append
+// are planned before the streaming loop, since they decide what is read.
+template <int DH, bool STEP, bool ORD, bool CROP = false>
 __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a) {
   __shared__ int pages[kMaxChunkPages];
   __shared__ int flag;
@@ -704,7 +963,8 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
   __shared__ float step_sn[16];       // fused step: scaled score of the new token per query head
   __shared__ float step_vn[DH];       // ... and its V row
   __shared__ int step_bad_page[kDecWaves];
-  __shared__ int step_plan_sh[2];     // ... the append commits; block popped for this request
+  __shared__ int step_plan_sh[3];     // ... the append commits; block popped for this request; its crop
+  __shared__ uint32_t dup_bm[STEP ? kDupBitmapWords : 1];  // the plan's duplicate-id check (one wave)
 
   const int c = blockIdx.x;
   int g = blockIdx.y, i = blockIdx.z;  // (request, kv head): grid position, or by length order
@@ -729,7 +989,10 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
 
   if constexpr (STEP) {
     if (i == a.n) {  // the commit workgroup; the rest of this grid row has nothing to do
-      if (c == 0 && g == 0 && w == 0) step_commit_wave(a);
+      if (c == 0 && g == 0 && w == 0) {
+        if constexpr (CROP) step_commit_wave_crop(a, dup_bm);
+        else step_commit_wave(a, dup_bm);
+      }
       return;
     }
     esink = nullptr;  // errors travel with the arrival
@@ -737,7 +1000,7 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     // append's plan needs, two round trips beside the other waves' chain of
     // this request's id, length and page ids; the plan itself is worked
     // out after the streaming loop, where it is first needed
-    if (w == kDecWaves - 1) step_plan_read1(a, pr);
+    if (w == kDecWaves - 1) step_plan_read1<CROP>(a, pr);
     if constexpr (ORD)
       if (ordered) order_pick(a, g, i, s_ord, L_ord, ord_key, ord_pick);
     s = ordered ? s_ord : a.seq_ids[i];
@@ -746,7 +1009,26 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     if (w == kDecWaves - 1) step_plan_read2(a, pr);
     L_pool = own_ok ? (ordered ? L_ord : a.lengths[s]) : 0;
     if (!own_ok || L_pool < 0 || L_pool > (a.max_blocks << bs_log2)) st = SM_ERR_EINVAL;
-    own_can = !frozen && st == 0 && (int64_t)L_pool + 1 <= a.cap;
+    if constexpr (CROP) {
+      // whether the crops and the append commit decides what this request
+      // attends over: its first L - c entries and the new row, or its
+      // unchanged cache; wave 3 works the plan out now and publishes it
+      if (w == kDecWaves - 1) {
+        PlanOutC po;
+        plan_crop(a, pr, po, dup_bm);
+        const int pop_i = request_value(po.pop, i), ck_i = request_value(pr.ck, i);
+        if (lane == 0) {
+          step_plan_sh[0] = po.ok;
+          step_plan_sh[1] = pop_i;
+          step_plan_sh[2] = ck_i;
+        }
+      }
+      lds_barrier();
+      own_can = step_plan_sh[0] != 0;  // (then every request passed its checks)
+      if (own_can) L_pool -= step_plan_sh[2];
+    } else {
+      own_can = !frozen && st == 0 && (int64_t)L_pool + 1 <= a.cap;
+    }
     if (st == 0) {  // chunked for the appended length whenever this request can append
       if (own_can && L_pool + 1 <= a.max_len) L = L_pool + 1;
       else {
@@ -853,17 +1135,21 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     }
   };
   auto step_plan_decide = [&]() __attribute__((always_inline)) {
-    if (w == kDecWaves - 1) {
-      PlanOut po;
-      plan_any(a, pr, po);
-      const int pop_i = request_value(po.pop, i);
-      if (lane == 0) {
-        step_plan_sh[0] = po.ok;
-        step_plan_sh[1] = pop_i;
+    if constexpr (CROP) {  // planned and published in the prologue
+      step_decide();
+    } else {
+      if (w == kDecWaves - 1) {
+        PlanOut po;
+        plan_any(a, pr, po, dup_bm);
+        const int pop_i = request_value(po.pop, i);
+        if (lane == 0) {
+          step_plan_sh[0] = po.ok;
+          step_plan_sh[1] = pop_i;
+        }
       }
+      lds_barrier();
+      step_decide();
     }
-    lds_barrier();
-    step_decide();
   };
   auto step_finish = [&]() __attribute__((always_inline)) {
     if (new_blk >= 0 && tid < DH) {  // the appended row of head g into its page
@@ -1394,11 +1680,11 @@ static int device_cus() {
 }
 
 // Workgroups of a bf16 decode kernel resident on one compute unit at once.
-template <int DH, bool STEP>
+template <int DH, bool STEP, bool CROP>
 static int bf16_occupancy() {
   static const int occ = [] {
     int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_split_bf16<DH, STEP, true>, kDecThreads, 0) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_split_bf16<DH, STEP, true, CROP>, kDecThreads, 0) !=
         hipSuccess)
       nb = 1;
     return nb > 0 ? nb : 1;
@@ -1419,10 +1705,27 @@ static sm_status decode_launch(const sm_paged_cache *c, DecodeArgs a, int n, hip
     if (cus > 0 && (int64_t)n * c->num_kv_heads > cus) {
       a.order_n = n;
       a.order_cus = cus;
-      a.order_occ = c->head_dim == 128 ? bf16_occupancy<128, STEP>() : bf16_occupancy<64, STEP>();
+      const bool d128 = c->head_dim == 128;
+      if (STEP && a.crop)
+        a.order_occ = d128 ? bf16_occupancy<128, STEP, STEP>() : bf16_occupancy<64, STEP, STEP>();
+      else
+        a.order_occ = d128 ? bf16_occupancy<128, STEP, false>() : bf16_occupancy<64, STEP, false>();
     }
   }
-  if (c->dtype == SM_BF16) {
+  if (c->dtype == SM_BF16 && STEP && a.crop) {
+    const bool ord = a.order_n > 0;
+    if (c->head_dim == 128) {
+      if (ord)
+        hipLaunchKernelGGL((decode_split_bf16<128, true, true, true>), grid, dim3(kDecThreads), 0, stream, a);
+      else
+        hipLaunchKernelGGL((decode_split_bf16<128, true, false, true>), grid, dim3(kDecThreads), 0, stream, a);
+    } else {
+      if (ord)
+        hipLaunchKernelGGL((decode_split_bf16<64, true, true, true>), grid, dim3(kDecThreads), 0, stream, a);
+      else
+        hipLaunchKernelGGL((decode_split_bf16<64, true, false, true>), grid, dim3(kDecThreads), 0, stream, a);
+    }
+  } else if (c->dtype == SM_BF16) {
     const bool ord = a.order_n > 0;
     if (c->head_dim == 128) {
       if (ord)
@@ -1464,7 +1767,8 @@ SM_API void sm_set_commit_wait_limit(int polls) {
 
 static sm_status decode_step_impl(const sm_paged_cache *c, const int32_t *seq_ids, int n, const void *K,
                                   const void *V, const void *q, int num_q_heads, float scale, int max_len,
-                                  void *out, void *ws, size_t ws_bytes, bool exact_ws, hipStream_t stream) {
+                                  void *out, void *ws, size_t ws_bytes, bool exact_ws, hipStream_t stream,
+                                  const int32_t *crop = nullptr) {
   if (n > kDecThreads) return SM_EINVAL;
   if (n > 0 && (!K || !V || !c || !c->free_stack || !c->free_top)) return SM_EINVAL;
   DecodeArgs a;
@@ -1473,6 +1777,7 @@ static sm_status decode_step_impl(const sm_paged_cache *c, const int32_t *seq_id
                                     kMaxPairs - 2, a, exact_ws);
   if (st != SM_OK || n == 0) return st;
   a.k_new = K;
+  a.crop = crop;
   a.v_new = V;
   a.free_stack = c->free_stack;
   a.free_top = c->free_top;
@@ -1491,6 +1796,15 @@ SM_API sm_status sm_decode_step(const sm_paged_cache *c, const int32_t *seq_ids,
                                 const void *V, const void *q, int num_q_heads, float scale, int max_len,
                                 void *out, void *ws, size_t ws_bytes, hipStream_t stream) {
   return decode_step_impl(c, seq_ids, n, K, V, q, num_q_heads, scale, max_len, out, ws, ws_bytes, false, stream);
+}
+
+SM_API sm_status sm_decode_merge_step(const sm_paged_cache *c, const int32_t *seq_ids, const int32_t *crop, int n,
+                                      const void *K, const void *V, const void *q, int num_q_heads, float scale,
+                                      int max_len, void *out, void *ws, size_t ws_bytes, hipStream_t stream) {
+  if (!c || c->dtype != SM_BF16) return SM_EINVAL;
+  if (n > 0 && !crop) return SM_EINVAL;
+  return decode_step_impl(c, seq_ids, n, K, V, q, num_q_heads, scale, max_len, out, ws, ws_bytes, false, stream,
+                          crop);
 }
 
 // ---------------------------------------------------------------------------

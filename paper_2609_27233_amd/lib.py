@@ -26,7 +26,7 @@ _P, _I, _L, _F, _Z = C.c_void_p, C.c_int, C.c_int64, C.c_float, C.c_size_t
 EXPORTED = ("sm_status_string", "sm_merge_workspace_bytes", "sm_merge_spans",
             "sm_merge_token_table", "sm_merge_spans_tabled",
             "sm_pack_spans", "sm_kv_rollback", "sm_kv_append",
-            "sm_decode_workspace_bytes", "sm_decode_attention", "sm_decode_step",
+            "sm_decode_workspace_bytes", "sm_decode_attention", "sm_decode_step", "sm_decode_merge_step",
             "sm_decode_step_noalloc_max_bytes", "sm_decode_step_noalloc", "sm_set_commit_wait_limit",
             "sm_prefill_attention", "sm_rules_build_workspace_bytes", "sm_rules_build",
             "sm_rules_lookup", "sm_match_prompt_workspace_bytes", "sm_match_prompt",
@@ -99,6 +99,9 @@ def load(path: str = LIB_PATH):
     L.sm_decode_step.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _P, _P, _I, _F,
                                  _I, _P, _P, _Z, _P]
     L.sm_decode_step.restype = _I
+    L.sm_decode_merge_step.argtypes = [C.POINTER(PagedCacheDesc), _P, _P, _I, _P, _P, _P, _I, _F,
+                                       _I, _P, _P, _Z, _P]
+    L.sm_decode_merge_step.restype = _I
     L.sm_decode_step_noalloc_max_bytes.argtypes = []
     L.sm_decode_step_noalloc_max_bytes.restype = _Z
     L.sm_decode_step_noalloc.argtypes = [C.POINTER(PagedCacheDesc), _P, _I, _P, _P, _P, _I, _F, _I, _P, _P]
@@ -306,6 +309,20 @@ def decode_step(cache: PagedCache, seq_ids, K, V, q, out, ws, max_len: int,
                                max_len, _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
                                _stream(stream))
     _check(st, "sm_decode_step")
+
+
+def decode_merge_step(cache: PagedCache, seq_ids, crop, K, V, q, out, ws, max_len: int,
+                      scale: Optional[float] = None, stream=None):
+    """The decode step at which spans complete: drop crop[i] cached entries
+    of each request, append its row and attend, in one launch (the same as
+    kv_rollback(cache, seq_ids, crop) then decode_step, made whole or not at
+    all)."""
+    n, Hq, D = q.shape
+    sc = D ** -0.5 if scale is None else scale
+    st = load().sm_decode_merge_step(C.byref(cache.desc), _ptr(seq_ids), _ptr(crop), n, _ptr(K), _ptr(V), _ptr(q),
+                                     Hq, sc, max_len, _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
+                                     _stream(stream))
+    _check(st, "sm_decode_merge_step")
 
 
 def decode_step_noalloc(cache: PagedCache, seq_ids, K, V, q, out, max_len: int,

@@ -79,18 +79,25 @@ class Lockstep:
         assert self.c.error_bits() == 0
         assert_same_state(self.c, self.oc, pools=pools)
 
-    def step(self, K, V, q, max_len, sample):
+    def step(self, K, V, q, max_len, sample, crop=None):
         """One fused decode step on the GPU (sm_decode_step: append a row per
-        sequence, attend); the oracle appends, and attends for the sampled
-        sequences (every query head of each)."""
+        sequence, attend; with `crop`, sm_decode_merge_step: first drop
+        crop[i] entries); the oracle appends (crop_append), and attends for
+        the sampled sequences (every query head of each)."""
         w = self.w
         n = w.batch
         if self.ws is None:
             self.ws = torch.zeros(sm.decode_workspace_bytes(n, w.num_q_heads, w.head_dim, max_len),
                                   dtype=torch.uint8, device=dev())
         out = torch.empty((n, w.num_q_heads, w.head_dim), dtype=w.torch_dtype, device=dev())
-        sm.decode_step(self.c, i32(np.arange(n)), K.to(dev()), V.to(dev()), q.to(dev()), out, self.ws, max_len)
-        assert self.oc.append(np.arange(n), np.arange(n + 1), wl.to_raw(K), wl.to_raw(V)) == self.orc.OK
+        if crop is None:
+            sm.decode_step(self.c, i32(np.arange(n)), K.to(dev()), V.to(dev()), q.to(dev()), out, self.ws, max_len)
+            assert self.oc.append(np.arange(n), np.arange(n + 1), wl.to_raw(K), wl.to_raw(V)) == self.orc.OK
+        else:
+            sm.decode_merge_step(self.c, i32(np.arange(n)), i32(crop), K.to(dev()), V.to(dev()), q.to(dev()), out,
+                                 self.ws, max_len)
+            assert self.oc.crop_append(np.arange(n), np.asarray(crop, np.int32), wl.to_raw(K),
+                                       wl.to_raw(V)) == self.orc.OK
         torch.cuda.synchronize()
         assert self.c.error_bits() == 0
         if len(sample):
@@ -243,7 +250,8 @@ def test_config1_tiny_f32_full_chain(orc):
 
 
 def _full_decode(orc, w, ls, emb, params, g, steps, max_len, pool_every, seqs_per_step):
-    """The configuration's whole decode run with the fused step: every
+    """The configuration's whole decode run with the fused steps (the merge
+    steps crop, append and attend in one sm_decode_merge_step): every
     decode-time merge's spans all checked, integer state after every step,
     pools every `pool_every` steps, attention of every sequence at the first
     step, every merge step and the last step, and of `seqs_per_step`
@@ -260,13 +268,13 @@ def _full_decode(orc, w, ls, emb, params, g, steps, max_len, pool_every, seqs_pe
             row_idx = rng.randint(0, w.vocab, size=int(offs[-1])).astype(np.int32)
             z = _gpu_merge(emb, row_idx, offs, params, w.h, w.torch_dtype)
             _merge_check(orc, emb, params, w.h, row_idx, offs, z, everyone, TOL[w.torch_dtype])
-            ls.rollback(everyone, n - 1)
         K = wl.randn((B, H, D), w.torch_dtype, g)
         V = wl.randn((B, H, D), w.torch_dtype, g)
         q = wl.randn((B, w.num_q_heads, D), w.torch_dtype, g)
         full = merging or s == 0 or s == steps - 1
         sample = everyone if full else np.sort(rng.choice(B, seqs_per_step, replace=False))
-        worst = max(worst, ls.step(K, V, q, max_len, sample))
+        # a merge step crops the span's n - 1 entries in the step's own launch
+        worst = max(worst, ls.step(K, V, q, max_len, sample, crop=(n - 1) if merging else None))
         ls.check_state(pools=(s % pool_every == pool_every - 1) or s == steps - 1)
         if s % 32 == 31 or s == steps - 1:
             say("step", s, "lengths", ls.oc.lengths[:4].tolist(), "worst attention rel_l2 so far", worst)
@@ -330,7 +338,7 @@ def test_prompt_compression_and_full_decode(orc, cid):
 def test_config4_ragged_contexts_with_frequent_rollback(orc):
     """Config 4: 128 sequences with contexts uniform in [512, 4096], all 256
     decode steps with the fused step, a decode-time merge (k ~ U{2,3,4},
-    n = k + 1 tokens at d = 3584, all 128 spans checked) and rollback every
+    n = k + 1 tokens at d = 3584, all 128 spans checked) and crop every
     4 steps, attention over the ragged cache (3 sequences x 28 heads per
     step, every sequence at merge steps and the first and last)."""
     w = wl.WORKLOADS[4]

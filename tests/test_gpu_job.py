@@ -7,8 +7,9 @@ batches on four streams, exactly as bench.py schedules them:
   128,256-row vocabulary, sm_merge_spans_tabled for the prompt spans and
   for every decode-time merge;
 * sm_pack_spans and the bulk sm_kv_append of the compressed prompts;
-* before every merge step, sm_kv_rollback of n - 1 entries per sequence;
-* every decode step one fused sm_decode_step launch per batch.
+* every decode step one fused launch per batch: sm_decode_step, or at a
+  merge step sm_decode_merge_step (crop n - 1 entries per sequence, append
+  the surrogate's row, attend).
 
 The job's test hook synchronizes after each phase and the oracle replays it:
 pack indices and packed rows bit for bit; 256 sampled prompt surrogates per
@@ -98,13 +99,16 @@ def test_bench_job_all_256_steps_on_four_streams(orc):
                 assert e <= tol, (s, lane, e)
             counts["decode_spans"] += lanes * B
             for r in range(R):
-                assert ocs[r].rollback(ids, m["n"] - 1) == orc.OK
-                meta(r)
+                meta(r)   # the crop comes with the step's launch
         else:
             j = s % job.nin
             check_attn = s == 0 or s in job.dmerge or s == w.decode_steps - 1
             for r in range(R):
-                assert ocs[r].append(ids, np.arange(B + 1), Kt[j], Vt[j]) == orc.OK
+                if s in job.dmerge:
+                    st = ocs[r].crop_append(ids, job.dmerge[s]["n"] - 1, Kt[j], Vt[j])
+                else:
+                    st = ocs[r].append(ids, np.arange(B + 1), Kt[j], Vt[j])
+                assert st == orc.OK
                 meta(r)
                 if check_attn:
                     st, ref = ocs[r].decode_attention(ids, q64[j], Hq, D ** -0.5)

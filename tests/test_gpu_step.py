@@ -407,3 +407,35 @@ def test_step_pairs_dealt_by_length(orc, n, H, Hq, D, hi):
         err = rel_l2_max(out.float().numpy(), ref)
         say("rel_l2_max", err)
         assert err <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dup", [None, (3, 69)])
+def test_many_sequence_slots_duplicate_check(orc, dup):
+    """More sequence slots (40,000) than the plan's LDS bitmap covers: the
+    duplicate-id check compares ids instead; 70 requests, with and without
+    a repeated id."""
+    dtype, Hq, H, D, bs = torch.bfloat16, 8, 2, 64, 16
+    rng = np.random.RandomState(4000 + (dup[1] if dup else 0))
+    n = 70
+    lens = list(rng.randint(0, 70, size=n))
+    oc, c = _cache(orc, rng, dtype, H, D, bs, lens, extra_seqs=40000 - n)
+    ids = rng.permutation(n).astype(np.int32)
+    ids[5] = 39999 - 7   # a high slot (empty sequence)
+    if dup:
+        ids[dup[1]] = ids[dup[0]]
+    K, V, q = _inputs(rng, dtype, n, H, Hq, D)
+    say("decode step, 40000 slots, repeated id", dup)
+    if dup:
+        snap = _snapshot(c)
+        st_d, ref = oc.decode_attention(ids, wl.to_f64(q), Hq, D ** -0.5)
+        out, ws = _gpu_step(c, ids, K, V, q, 80)
+        _assert_unchanged(c, snap)
+        assert c.error_bits() == sm.ERR_EINVAL
+    else:
+        st_a, st_d, ref = _oracle_step(orc, oc, ids, K, V, q, Hq)
+        assert st_a == orc.OK
+        out, ws = _gpu_step(c, ids, K, V, q, 80)
+        assert c.error_bits() == 0
+        assert_same_state(c, oc)
+    _counters_clear(ws)
+    assert rel_l2_max(out.float().numpy(), ref) <= TOL[dtype]

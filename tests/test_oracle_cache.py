@@ -190,3 +190,82 @@ def test_rope_offsets_unchanged_before_the_span(orc):
     assert np.isclose(q1[5, 0] @ k1[4, 0], q2[5, 0] @ k2[4, 0], rtol=1e-12)
     # a pair across the span is shortened by one position
     assert not np.isclose(q1[5, 0] @ k1[0, 0], q2[5, 0] @ k2[0, 0], rtol=1e-9)
+
+
+def test_crop_append_against_list_model(orc):
+    """crop_append (the decode-time merge update as one step): every request
+    goes from L to L - k + 1 entries, its logical K/V is its first L - k rows
+    plus the new one, and blocks are conserved; when any check fails the
+    whole cache is as before, even where the crop alone would have
+    succeeded."""
+    rng = np.random.RandomState(77)
+    H, D, bs, NB, S = 2, 64, 16, 24, 6
+    c = _cache(orc, H=H, D=D, bs=bs, NB=NB, S=S, MB=12, order=rng.permutation(NB).astype(np.int32))
+    model = {s: [] for s in range(S)}
+    n_ok = n_fail = 0
+    for step in range(200):
+        ids = rng.choice(S, size=rng.randint(1, S + 1), replace=False).astype(np.int32)
+        if rng.rand() < 0.3:  # grow
+            m = rng.randint(0, 40, size=len(ids))
+            offs = np.concatenate([[0], np.cumsum(m)]).astype(np.int32)
+            K, V = _rows(rng, offs[-1], H, D), _rows(rng, offs[-1], H, D)
+            if c.append(ids, offs, K, V) == orc.OK:
+                for i, s in enumerate(ids):
+                    model[s] += [(K[r], V[r]) for r in range(offs[i], offs[i + 1])]
+            continue
+        k = np.array([rng.randint(0, min(len(model[s]), 9) + 1) if rng.rand() < 0.9 else len(model[s])
+                      for s in ids], np.int32)
+        if rng.rand() < 0.05:
+            k[0] = len(model[ids[0]]) + 1          # crop longer than the cache
+        K, V = _rows(rng, len(ids), H, D), _rows(rng, len(ids), H, D)
+        snap = _snapshot(c)
+        st = c.crop_append(ids, k, K, V)
+        if any(kk > len(model[s]) for s, kk in zip(ids, k)):
+            assert st == orc.ERANGE
+        elif any(len(model[s]) - kk + 1 > 12 * bs for s, kk in zip(ids, k)):
+            assert st == orc.ERANGE
+        else:
+            used = sum(-(-(len(model[s]) - kk + (s in ids and 1)) // bs) if s in ids else -(-len(model[s]) // bs)
+                       for s, kk in zip(list(range(S)), [dict(zip(ids, k)).get(s, 0) for s in range(S)]))
+            assert st == (orc.OK if used <= NB else orc.ENOMEM)
+        if st == orc.OK:
+            n_ok += 1
+            for i, s in enumerate(ids):
+                model[s] = model[s][:len(model[s]) - k[i]] + [(K[i], V[i])]
+        else:
+            n_fail += 1
+            assert _same(snap, _snapshot(c))
+        mapped = []
+        for s in range(S):
+            L = len(model[s])
+            assert c.lengths[s] == L
+            nb = -(-L // bs)
+            mapped += c.block_table[s, :nb].tolist()
+            assert np.all(c.block_table[s, nb:] == -1)
+            if L:
+                Kl, Vl = c.logical_kv(s)
+                np.testing.assert_array_equal(Kl, np.stack([r[0] for r in model[s]]))
+                np.testing.assert_array_equal(Vl, np.stack([r[1] for r in model[s]]))
+        top = int(c.free_top[0])
+        assert sorted(mapped + c.free_stack[:top].tolist()) == list(range(NB))
+    assert n_ok > 50 and n_fail > 5
+
+
+def test_crop_append_failure_after_a_good_crop_restores(orc):
+    """The append fails for want of a block after the crop succeeded: the
+    two separate calls would leave the crop applied; the one update leaves
+    nothing."""
+    rng = np.random.RandomState(5)
+    c = _cache(orc, NB=6, MB=4, S=4)   # filled: no free block
+    assert c.append([0, 1], [0, 32, 64], _rows(rng, 64, 2, 64), _rows(rng, 64, 2, 64)) == orc.OK
+    assert c.append([2], [0, 32], _rows(rng, 32, 2, 64), _rows(rng, 32, 2, 64)) == orc.OK
+    snap = _snapshot(c)
+    # request 0 crops 1 (no block freed); requests 1 and 2 end pages and need 2 blocks, none free
+    st = c.crop_append([0, 1, 2], [1, 0, 0], _rows(rng, 3, 2, 64), _rows(rng, 3, 2, 64))
+    assert st == orc.ENOMEM
+    assert _same(snap, _snapshot(c))
+    # a crop that frees a page makes room: request 0 frees its second page, request 1 pops it
+    st = c.crop_append([0, 1], [17, 0], _rows(rng, 2, 2, 64), _rows(rng, 2, 2, 64))
+    assert st == orc.OK
+    assert c.lengths[0] == 16 and c.lengths[1] == 33
+    assert c.block_table[1, 2] == snap[2][0, 1]   # the block request 0 gave up
