@@ -122,38 +122,41 @@ __device__ __forceinline__ int dealt_rank(int b, int W, int cus, int occ) {
 // The (request, kv head) of grid position (row i, head column g) under the
 // length order; s_out / L_out: the request's sequence id and its cached
 // length (-1 for an id out of range).  All threads take part: order_n is at
-// most the workgroup size, one request per thread.  `key` holds order_n
-// ints of LDS, `pick` three.
+// most the workgroup size.  Request j's sort key is (length, then the
+// smaller index) packed into one 64-bit integer, so that its rank is the
+// number of larger keys; P = 256 / n (at most 4) threads count over
+// contiguous shares of the keys and add their counts.  LDS: `key` order_n
+// 64-bit keys, `sid` order_n ints, `pick` one int.
 __device__ __forceinline__ void order_pick(const DecodeArgs &a, int &g, int &i, int &s_out, int &L_out,
-                                           int *key, int *pick) {
+                                           int64_t *key, int *sid, int *pick) {
   const int n = a.order_n, tid = threadIdx.x;
   const int rho = dealt_rank(i * a.Hkv + g, n * a.Hkv, a.order_cus, a.order_occ);
   const int k = rho / a.Hkv;
   g = rho - k * a.Hkv;
-  int sj = -1, kj = -1;
   if (tid < n) {
-    sj = a.seq_ids[tid];
-    kj = (sj >= 0 && sj < a.max_seqs) ? a.lengths[sj] : -1;
-    key[tid] = kj;
+    const int sj = a.seq_ids[tid];
+    const int kj = (sj >= 0 && sj < a.max_seqs) ? a.lengths[sj] : -1;
+    key[tid] = (int64_t)kj * 512 + (511 - tid);
+    sid[tid] = sj;
   }
   lds_barrier();
-  if (tid < n) {
-    int r = 0;
+  const int P = n <= 64 ? 4 : n <= 128 ? 2 : 1;
+  const int j = tid / P, part = tid - j * P;
+  int r = 0;
+  if (j < n) {
+    const int64_t kj = key[j];
+    const int m0 = part * n / P, m1 = (part + 1) * n / P;
 #pragma unroll 8
-    for (int m = 0; m < n; ++m) {
-      const int km = key[m];
-      r += (km > kj) | ((km == kj) & (m < tid));
-    }
-    if (r == k) {  // ranks are a permutation of 0 .. n - 1: exactly one thread
-      pick[0] = tid;
-      pick[1] = sj;
-      pick[2] = kj;
-    }
+    for (int m = m0; m < m1; ++m) r += key[m] > kj;
   }
+  // the P threads of a request are consecutive lanes of one wave
+  if (P >= 2) r += __shfl_xor(r, 1, kWave);
+  if (P >= 4) r += __shfl_xor(r, 2, kWave);
+  if (j < n && part == 0 && r == k) *pick = j;  // ranks are a permutation of 0 .. n - 1: exactly one
   lds_barrier();
-  i = pick[0];
-  s_out = pick[1];
-  L_out = pick[2];
+  i = *pick;
+  s_out = sid[i];
+  L_out = (int)((key[i] - (511 - i)) / 512);
 }
 
 // Load the block ids of logical pages [lp0, lp0 + npages) into LDS and
@@ -973,7 +976,8 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
   int s = 0, L = 0, st = 0, L_pool = 0;  // chunking covers [0, L), the pool holds [0, L_pool)
   const bool ordered = ORD && i < a.order_n;  // (the step's commit row is not)
   int s_ord = 0, L_ord = 0;
-  __shared__ int ord_key[ORD ? kDecThreads : 1], ord_pick[3];
+  __shared__ int64_t ord_key[ORD ? kDecThreads : 1];
+  __shared__ int ord_sid[ORD ? kDecThreads : 1], ord_pick[1];
   int nc = 0, chunk = 0, t0 = 0, t1 = 0, lp0 = 0, npages = 0;
   bool work = false, pages_ok = true;
 
@@ -1002,7 +1006,7 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     // out after the streaming loop, where it is first needed
     if (w == kDecWaves - 1) step_plan_read1<CROP>(a, pr);
     if constexpr (ORD)
-      if (ordered) order_pick(a, g, i, s_ord, L_ord, ord_key, ord_pick);
+      if (ordered) order_pick(a, g, i, s_ord, L_ord, ord_key, ord_sid, ord_pick);
     s = ordered ? s_ord : a.seq_ids[i];
     const int frozen = *a.err != 0;
     const bool own_ok = s >= 0 && s < a.max_seqs;
@@ -1087,7 +1091,7 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_bf16(DecodeArgs a
     for (int ww = 0; ww < kDecWaves; ++ww) pages_ok = pages_ok && !step_bad_page[ww];
   } else {
     if constexpr (ORD)
-      if (ordered) order_pick(a, g, i, s_ord, L_ord, ord_key, ord_pick);
+      if (ordered) order_pick(a, g, i, s_ord, L_ord, ord_key, ord_sid, ord_pick);
     s = ordered ? s_ord : a.seq_ids[i];
     st = seq_status(a, s, L, ordered, L_ord);
     L_pool = L;
