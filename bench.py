@@ -50,8 +50,8 @@ METRIC = "decode-attention tokens/s + achieved HBM GB/s over span-compacted KV c
 # WRITE_SIZE runs (see profiles/decode_step_llama3-8b-layer.md): scaled
 # measured bytes per launch divided by the algorithmic bytes of the same
 # launches.  Valid only for the kernel source it was measured on.
-TRAFFIC_RATIO = 1.0155
-TRAFFIC_SOURCE_SHA256 = {"decode_attn.hip": "e1df1f0ce4ea31eb1dcf9c19adad5018a99e50c90eebf9f42d5e82c2b7f5177d", "common.hpp": "b33d848d212d0d3e660d0e361606225f38e6024217e8cff49c2cdf89b79a2751"}
+TRAFFIC_RATIO = 1.0153
+TRAFFIC_SOURCE_SHA256 = {"decode_attn.hip": "7ebac19459e1d185ca656f1d77649011df215d63ea84b769a15ccf7f6932dd37", "common.hpp": "b33d848d212d0d3e660d0e361606225f38e6024217e8cff49c2cdf89b79a2751"}
 
 
 def log(*a):
