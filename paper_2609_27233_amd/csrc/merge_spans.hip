@@ -157,11 +157,16 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_nt_gelu(const uint16_t *__re
 // LDS reads and the ring refills with the MFMAs.
 //
 // LDS layout of one operand stage: 256 rows x 64 bytes as 16-byte slots
-// row * 4 + (chunk ^ ((row >> 1) & 3)); the swizzle keeps the fragment
-// reads free of bank conflicts.  A direct-to-LDS load writes 64
-// consecutive slots (one per lane), so lane l of a load covers row
-// base + l / 4, slot chunk l % 4, and fetches global chunk
-// (l % 4) ^ swizzle(row).
+// row * 4 + (chunk ^ ((row >> 2) & 3)).  A 16-byte LDS read serves 16
+// lanes per cycle from 64 banks (256 bytes): the 16 lanes of a fragment
+// read take rows r .. r + 15 of one chunk, and the swizzle puts them in 16
+// distinct 16-byte bank groups (row % 4 picks the 64-byte quarter, the
+// swizzled chunk the slot within it), so the reads are free of bank
+// conflicts (SQ_LDS_BANK_CONFLICT = 0; a swizzle by (row >> 1) & 3 left
+// rows r and r + 8 in one group, 4 conflict cycles per read).  A
+// direct-to-LDS load writes 64 consecutive slots (one per lane), so lane l
+// of a load covers row base + l / 4, slot chunk l % 4, and fetches global
+// chunk (l % 4) ^ swizzle(row).
 //
 // Tile order: the hardware hands workgroup b to XCD b % 8; XCD x takes the
 // logical tiles [x * per_xcd, (x + 1) * per_xcd) in groups of kGroupM row
@@ -172,7 +177,7 @@ constexpr int kLM = 256, kLN = 256, kLK = 32, kLStages = 4, kLThreads = 512, kGr
 constexpr int kLStageBytes = kLM * kLK * 2;  // per operand
 constexpr int kLLdsBytes = 2 * kLStages * kLStageBytes;
 
-__device__ __forceinline__ int lds_swz(int row) { return (row >> 1) & 3; }
+__device__ __forceinline__ int lds_swz(int row) { return (row >> 2) & 3; }
 
 // s_waitcnt with vmcnt = N, lgkmcnt = 0, expcnt left open
 template <int N>
