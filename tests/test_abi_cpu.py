@@ -66,6 +66,7 @@ def test_cache_descriptor_checks(L, kw):
     assert L.sm_kv_append(C.byref(d), 1, 1, 1, 1, 1, 1, None) == sm.SM_EINVAL
     assert L.sm_decode_attention(C.byref(d), 1, 1, 1, 8, 1.0, 16, 1, 1, 1 << 30, None) == sm.SM_EINVAL
     assert L.sm_decode_step(C.byref(d), 1, 1, 1, 1, 1, 8, 1.0, 16, 1, 1, 1 << 30, None) == sm.SM_EINVAL
+    assert L.sm_decode_merge_step(C.byref(d), 1, 1, 1, 1, 1, 1, 8, 1.0, 16, 1, 1, 1 << 30, None) == sm.SM_EINVAL
     assert L.sm_prefill_attention(C.byref(d), 1, 1, 1, 16, 1, 8, 1.0, 16, 1, None) == sm.SM_EINVAL
 
 
@@ -108,6 +109,13 @@ def test_request_count_and_workspace_checks(L):
     assert L.sm_decode_step(C.byref(d), 1, 1, 1, None, 1, 32, 1.0, 256, 1, 1, 1 << 30, None) == sm.SM_EINVAL
     assert L.sm_decode_step(C.byref(d), 1, 1, 1, 1, 1, 32, 1.0, 256, 1, 1, need - 1, None) == sm.SM_EINVAL
     assert L.sm_decode_step(C.byref(d), 1, 1, 1, 1, 1, 32, 1.0, 257, 1, 1, 1 << 30, None) == sm.SM_EINVAL
+    # the merge step: the same rules, a crop array required, bf16 caches only
+    assert L.sm_decode_merge_step(C.byref(d), 1, 1, 0, None, None, 1, 32, 1.0, 256, 1, 1, 1 << 30, None) == sm.SM_OK
+    assert L.sm_decode_merge_step(C.byref(d), 1, None, 1, 1, 1, 1, 32, 1.0, 256, 1, 1, 1 << 30, None) == sm.SM_EINVAL
+    assert L.sm_decode_merge_step(C.byref(d), 1, 1, 257, 1, 1, 1, 32, 1.0, 256, 1, 1, 1 << 30, None) == sm.SM_EINVAL
+    assert L.sm_decode_merge_step(C.byref(d), 1, 1, 1, 1, 1, 1, 32, 1.0, 256, 1, 1, need - 1, None) == sm.SM_EINVAL
+    f = _desc(dtype=sm.SM_F32)
+    assert L.sm_decode_merge_step(C.byref(f), 1, 1, 1, 1, 1, 1, 32, 1.0, 256, 1, 1, 1 << 30, None) == sm.SM_EINVAL
 
 
 def test_merge_argument_checks(L):
