@@ -281,25 +281,6 @@ __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
       FB[2 + j] = *(const u32x4_t *)(lb_ + j * 2048 + fo1);                                \
     }                                                                                      \
   }
-  // swapped operands: the MFMA computes D[n][m], so a lane ends up holding
-  // four consecutive output columns of one row
-#define SM_MMA(FA, FB)                                                                     \
-  _Pragma("unroll") for (int ks = 0; ks < 2; ++ks)                                         \
-  _Pragma("unroll") for (int i = 0; i < 4; ++i)                                            \
-  _Pragma("unroll") for (int j = 0; j < 2; ++j)                                            \
-    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(FB[2 * ks + j]),         \
-                                                        as_bf16x8(FA[4 * ks + i]), acc[i][j], 0, 0, 0);
-  // 16 MFMAs, 12 fragment reads and 4 ring loads per wave and k-tile
-#define SM_INTERLEAVE()                                                                    \
-  {                                                                                        \
-    _Pragma("unroll") for (int g = 0; g < 12; ++g) {                                       \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                   \
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                                   \
-      if (g < 4) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                        \
-    }                                                                                      \
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                     \
-  }
-
   // Ring: k-tile t lives in stage t % 4.  The step that multiplies k-tile kt
   // waits for kt + 1, passes the barrier (after which no wave still reads
   // the stage of kt), refills that stage with k-tile kt + 4 and reads the
@@ -313,28 +294,46 @@ __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
   wait_vmcnt_lgkm0<4 * (kLStages - 1)>();
   __builtin_amdgcn_s_barrier();
   SM_READ_FRAGS(0, f0a, f0b);
-  for (int kt = 0; kt < nk; kt += 2) {
-    wait_vmcnt_lgkm0<4 * (kLStages - 2)>();
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-    refill(min(kt + kLStages, nk - 1), kt & (kLStages - 1));
-    SM_READ_FRAGS(kt + 1, f1a, f1b);
-    SM_MMA(f0a, f0b);
-    SM_INTERLEAVE();
-    __builtin_amdgcn_sched_barrier(0);
-    wait_vmcnt_lgkm0<4 * (kLStages - 2)>();
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-    refill(min(kt + 1 + kLStages, nk - 1), (kt + 1) & (kLStages - 1));
-    SM_READ_FRAGS(kt + 2, f0a, f0b);  // past the end: reads a stale stage, unused
-    SM_MMA(f1a, f1b);
-    SM_INTERLEAVE();
-    __builtin_amdgcn_sched_barrier(0);
+  auto refill_q = [&](int kt, int stage, int q) {  // load q (A, B, A, B) of refill(kt, stage)
+    const int ko = kt * kLK, u = q >> 1;
+    if (q & 1) load_to_lds16(pb[u] + ko, sb + stage * kLStageBytes + (u * 8 + w) * 1024);
+    else load_to_lds16(pa[u] + ko, sa + stage * kLStageBytes + (u * 8 + w) * 1024);
+  };
+  // One step on k-tile KT, whose fragments are in FA / FB: 16 MFMAs, each
+  // followed by one of the 12 fragment reads of k-tile KT + 1 (into GA / GB)
+  // and one of the 4 ring loads, in this fixed order (a scheduling barrier
+  // after each group).  The MFMAs go k step by k step over the 8
+  // accumulators, so two MFMAs into one accumulator are 8 apart; left to
+  // itself the scheduler put some of them back to back.  Swapped operands:
+  // the MFMA computes D[n][m], so a lane ends up holding four consecutive
+  // output columns of one row.
+#define SM_STEP(KT, FA, FB, GA, GB)                                                                  \
+  {                                                                                                  \
+    wait_vmcnt_lgkm0<4 * (kLStages - 2)>();                                                          \
+    __builtin_amdgcn_s_barrier();                                                                    \
+    __builtin_amdgcn_sched_barrier(0);                                                               \
+    const int rk_ = min((KT) + kLStages, nk - 1), rs_ = (KT) & (kLStages - 1);                        \
+    const uint8_t *la_ = sa + (((KT) + 1) & (kLStages - 1)) * kLStageBytes + a_off;                  \
+    const uint8_t *lb_ = sb + (((KT) + 1) & (kLStages - 1)) * kLStageBytes + b_off;                  \
+    _Pragma("unroll") for (int g = 0; g < 16; ++g) {                                                 \
+      const int ks = g >> 3, i = (g >> 1) & 3, j = g & 1;                                            \
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(FB[2 * ks + j]),                 \
+                                                          as_bf16x8(FA[4 * ks + i]), acc[i][j], 0, 0, 0); \
+      if (g < 8)                                                                                     \
+        GA[g] = *(const u32x4_t *)(la_ + (g & 3) * 2048 + ((g >> 2) ? fo1 : fo0));                   \
+      else if (g < 12)                                                                               \
+        GB[g - 8] = *(const u32x4_t *)(lb_ + ((g - 8) & 1) * 2048 + (((g - 8) >> 1) ? fo1 : fo0));   \
+      if (g < 4) refill_q(rk_, rs_, g);                                                              \
+      __builtin_amdgcn_sched_barrier(0);                                                             \
+    }                                                                                                \
   }
+  for (int kt = 0; kt < nk; kt += 2) {
+    SM_STEP(kt, f0a, f0b, f1a, f1b);
+    SM_STEP(kt + 1, f1a, f1b, f0a, f0b);  // past the end: reads a stale stage, unused
+  }
+#undef SM_STEP
   wait_vmcnt_lgkm0<0>();
 #undef SM_READ_FRAGS
-#undef SM_MMA
-#undef SM_INTERLEAVE
 
   // 32x32 result layout (swapped): register 4 g + e of tile (i, j) holds
   // C[row 32 i + r32][col 32 j + 8 g + 4 h2 + e]
@@ -897,11 +896,279 @@ __global__ __launch_bounds__(kPoolWaves * 64) void pool_rows_kernel(const T *__r
   }
 }
 
+// Pooling, column-slice form for d = 4 * 64 * CPL * (16 / sizeof(T)):
+// persistent workgroups of four waves, each taking spans blockIdx.x,
+// blockIdx.x + gridDim.x, ...  Wave w owns columns [w d/4, (w + 1) d/4);
+// lane l holds the 16-byte groups c * 64 + l (c < CPL) of that slice of
+// every row.  So the slice's score weights q_j g_j stay in registers for
+// the whole kernel, a span's rows (up to kPoolResident of them) stay in
+// registers from the scores to the weighted sum, and the only data crossing
+// waves are a few sums per row in LDS.
+//
+// With the shift K_rw = the slice's first element of row r, wave w forms
+//   S1 = sum (x - K),  S2 = sum (x - K)^2,  T_h = sum_{j in head h} q_j g_j (x_j - K)
+// over its slice.  The four slices' (S1, S2) combine by the pairwise
+// update of Chan, Golub and LeVeque into the row's mean mu_r and
+// inv_r = 1 / sqrt(var_r + eps), and the score of head h is
+//   (inv_r sum_w [T_wh + (K_rw - mu_r) C_wh] + D_h) / sqrt(dh),
+//   C_wh = sum_{j in h, slice w} q_j g_j,  D_h = sum_{j in h} q_j beta_j,
+// i.e. q_h . LN_kv(x_r)_h / sqrt(dh).  With a_rh = alpha_rh inv_r (alpha the
+// per-head softmax over the span's rows) the pooled column j is
+//   g_j (sum_r a_rh (x_rj - K_rw) - E_wh) + beta_j,  E_wh = sum_r a_rh (mu_r - K_rw),
+// which is sum_r alpha_rh LN_kv(x_r)_j because each head's alphas sum to one.
+// The shifts keep the sums free of cancellation when a row's values sit
+// far from zero.
+constexpr int kPoolResident = 4;  // rows per group held in registers
+constexpr int kSliceHeads = 5;    // heads meeting one quarter of the columns (h <= 16, d/h a multiple of 64)
+
+template <typename T, int CPL>
+__global__ __launch_bounds__(256, 2) void pool_slices_kernel(const T *__restrict__ G1, const int32_t *__restrict__ gidx,
+                                                          int64_t g_rows, const int32_t *__restrict__ span_offsets,
+                                                          int num_spans, int total_rows, const T *__restrict__ Q,
+                                                          const T *__restrict__ g_kv, const T *__restrict__ beta_kv,
+                                                          float eps, int d, int h, T *__restrict__ cout,
+                                                          int32_t *err) {
+  constexpr int VN = Vec<T>::N;
+  __shared__ float sh_k[kMaxSpanLen][4], sh_s1[kMaxSpanLen][4], sh_s2[kMaxSpanLen][4];
+  __shared__ float sh_t[kMaxSpanLen][4][kSliceHeads];
+  __shared__ float sh_a[kMaxSpanLen][kMaxHeads];
+  __shared__ float sh_mu[kMaxSpanLen], sh_inv[kMaxSpanLen];
+  __shared__ float sh_c[4][kSliceHeads], sh_dq[4][kSliceHeads];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int slice = d >> 2, dh = d / h;
+  const int hf = (w * slice) / dh, nh = (w * slice + slice - 1) / dh - hf + 1;  // heads meeting this slice
+  const int c0 = w * slice + lane * VN;                                             // column of group 0
+  int hd[CPL];  // head of group c, counted from hf
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) hd[c] = (c0 + c * 64 * VN) / dh - hf;
+
+  float wq[CPL][VN];  // q_j g_j
+  {
+    float cs[kSliceHeads], ds[kSliceHeads];
+#pragma unroll
+    for (int hs = 0; hs < kSliceHeads; ++hs) cs[hs] = ds[hs] = 0.f;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const int col = c0 + c * 64 * VN;
+      float qf[VN], gf[VN], bf[VN];
+      unpack_vec<T>(*(const u32x4_t *)(Q + col), qf);
+      unpack_vec<T>(*(const u32x4_t *)(g_kv + col), gf);
+      unpack_vec<T>(*(const u32x4_t *)(beta_kv + col), bf);
+      float cc = 0.f, dd = 0.f;
+#pragma unroll
+      for (int e = 0; e < VN; ++e) {
+        wq[c][e] = qf[e] * gf[e];
+        cc += wq[c][e];
+        dd += qf[e] * bf[e];
+      }
+#pragma unroll
+      for (int hs = 0; hs < kSliceHeads; ++hs)
+        if (hd[c] == hs) {
+          cs[hs] += cc;
+          ds[hs] += dd;
+        }
+    }
+#pragma unroll
+    for (int hs = 0; hs < kSliceHeads; ++hs)
+      if (hs < nh) {  // wave-uniform
+        const float cw = wave_sum(cs[hs]), dw = wave_sum(ds[hs]);
+        if (lane == 0) {
+          sh_c[w][hs] = cw;
+          sh_dq[w][hs] = dw;
+        }
+      }
+  }
+  const float inv_sqrt_dh = 1.0f / sqrtf((float)dh), n_slice = (float)slice;
+
+  for (int s = blockIdx.x; s < num_spans; s += gridDim.x) {
+    T *dst = cout + (int64_t)s * d;
+    const int r0 = span_offsets[s], r1 = span_offsets[s + 1];
+    const int n = r1 - r0;
+    bool ok = n >= 1 && n <= kMaxSpanLen && r0 >= 0 && r1 <= total_rows;
+    if (s == 0 && r0 != 0) ok = false;
+    if (s == num_spans - 1 && r1 != total_rows) ok = false;
+    if (!ok) {  // (uniform over the workgroup)
+      if (tid == 0) set_err(err, SM_ERR_EINVAL);
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) *(u32x4_t *)(dst + c0 + c * 64 * VN) = u32x4_t{0u, 0u, 0u, 0u};
+      continue;
+    }
+    auto load_group = [&](u32x4_t (&xr)[kPoolResident][CPL], int g0, int nr) {
+#pragma unroll
+      for (int rr = 0; rr < kPoolResident; ++rr)
+        if (rr < nr) {
+          const T *row = g1_row(G1, gidx, g_rows, r0 + g0 + rr, d, err) + c0;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) xr[rr][c] = *(const u32x4_t *)(row + c * 64 * VN);
+        }
+    };
+    // slice sums of every row
+    u32x4_t xr[kPoolResident][CPL];
+    for (int g0 = 0; g0 < n; g0 += kPoolResident) {
+      const int nr = min(kPoolResident, n - g0);
+      load_group(xr, g0, nr);
+#pragma unroll
+      for (int rr = 0; rr < kPoolResident; ++rr)
+        if (rr < nr) {
+          const int r = g0 + rr;
+          float xk[VN];
+          unpack_vec<T>(xr[rr][0], xk);
+          const float K = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(xk[0])));
+          float s1 = 0.f, s2 = 0.f, tc[CPL];
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) {
+            float x[VN];
+            unpack_vec<T>(xr[rr][c], x);
+            float t = 0.f;
+#pragma unroll
+            for (int e = 0; e < VN; ++e) {
+              const float dx = x[e] - K;
+              s1 += dx;
+              s2 = fmaf(dx, dx, s2);
+              t = fmaf(wq[c][e], dx, t);
+            }
+            tc[c] = t;
+          }
+          s1 = wave_sum(s1);
+          s2 = wave_sum(s2);
+#pragma unroll
+          for (int hs = 0; hs < kSliceHeads; ++hs)
+            if (hs < nh) {
+              float t = 0.f;
+#pragma unroll
+              for (int c = 0; c < CPL; ++c) t += hd[c] == hs ? tc[c] : 0.f;
+              t = wave_sum(t);
+              if (lane == 0) sh_t[r][w][hs] = t;
+            }
+          if (lane == 0) {
+            sh_k[r][w] = K;
+            sh_s1[r][w] = s1;
+            sh_s2[r][w] = s2;
+          }
+        }
+    }
+    lds_barrier();
+    // row statistics, scores and the per-head softmax: thread hh < h takes head hh
+    if (tid < h) {
+      const int hh = tid, wf = (hh * dh) / slice, wl = (hh * dh + dh - 1) / slice;
+      float m = -INFINITY;
+      for (int r = 0; r < n; ++r) {
+        float mw[4], mean = 0.f, m2 = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < 4; ++ww) {
+          const float a1 = sh_s1[r][ww];
+          mw[ww] = sh_k[r][ww] + a1 / n_slice;
+          mean += mw[ww];
+          m2 += sh_s2[r][ww] - a1 * (a1 / n_slice);
+        }
+        mean *= 0.25f;
+#pragma unroll
+        for (int ww = 0; ww < 4; ++ww) m2 += n_slice * (mw[ww] - mean) * (mw[ww] - mean);
+        const float inv = 1.0f / sqrtf(fmaxf(m2, 0.f) / d + eps);
+        float t = 0.f, dq = 0.f;
+        for (int ww = wf; ww <= wl; ++ww) {
+          const int hs = hh - (ww * slice) / dh;
+          t += sh_t[r][ww][hs] + (sh_k[r][ww] - mean) * sh_c[ww][hs];
+          dq += sh_dq[ww][hs];
+        }
+        const float sc = (inv * t + dq) * inv_sqrt_dh;
+        sh_a[r][hh] = sc;
+        m = fmaxf(m, sc);
+        sh_mu[r] = mean;  // the same value from every head's thread
+        sh_inv[r] = inv;
+      }
+      float z = 0.f;
+      for (int r = 0; r < n; ++r) {
+        const float e = expf(sh_a[r][hh] - m);
+        sh_a[r][hh] = e;
+        z += e;
+      }
+      const float iz = 1.0f / z;
+      for (int r = 0; r < n; ++r) sh_a[r][hh] = sh_a[r][hh] * iz * sh_inv[r];
+    }
+    lds_barrier();
+    // weighted sum over this wave's slice (the gain and bias are re-read,
+    // from cache, rather than held in registers across the span loop)
+    u32x4_t gp[CPL], bp[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      gp[c] = *(const u32x4_t *)(g_kv + c0 + c * 64 * VN);
+      bp[c] = *(const u32x4_t *)(beta_kv + c0 + c * 64 * VN);
+    }
+    float E = 0.f;
+    if (lane < nh)
+      for (int r = 0; r < n; ++r) E += sh_a[r][hf + lane] * (sh_mu[r] - sh_k[r][w]);
+    float acc[CPL][VN];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c)
+#pragma unroll
+      for (int e = 0; e < VN; ++e) acc[c][e] = 0.f;
+    for (int g0 = 0; g0 < n; g0 += kPoolResident) {
+      const int nr = min(kPoolResident, n - g0);
+      if (n > kPoolResident) load_group(xr, g0, nr);  // else the rows are still held
+#pragma unroll
+      for (int rr = 0; rr < kPoolResident; ++rr)
+        if (rr < nr) {
+          const int r = g0 + rr;
+          const float K = sh_k[r][w];
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) {
+            const float a = sh_a[r][hf + hd[c]];
+            float x[VN];
+            unpack_vec<T>(xr[rr][c], x);
+#pragma unroll
+            for (int e = 0; e < VN; ++e) acc[c][e] = fmaf(a, x[e] - K, acc[c][e]);
+          }
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const float ec = __shfl(E, hd[c]);
+      float gf[VN], bf[VN], y[VN];
+      unpack_vec<T>(gp[c], gf);
+      unpack_vec<T>(bp[c], bf);
+#pragma unroll
+      for (int e = 0; e < VN; ++e) y[e] = fmaf(gf[e], acc[c][e] - ec, bf[e]);
+      store_vec(dst + c0 + c * 64 * VN, y);
+    }
+  }
+}
+
+// Resident workgroups of a pooling kernel over the whole device (looked up
+// once per kernel), for the persistent grid.
+template <typename K>
+static int resident_blocks(K kernel, int threads) {
+  static const int nb = [&] {
+    int dev = 0, cus = 0, occ = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, threads, 0) != hipSuccess || occ <= 0) occ = 1;
+    return cus * occ;
+  }();
+  return nb;
+}
+
 template <typename T>
 static hipError_t launch_pool(const T *G1, const int32_t *gidx, int64_t g_rows, const int32_t *span_offsets,
                               int num_spans, int total_rows, const T *Q, const T *g_kv, const T *beta_kv, float eps,
                               int d, int h, T *cout, int32_t *err, hipStream_t stream) {
   constexpr int VN = Vec<T>::N;
+  const int cpl = d % (256 * VN) == 0 ? d / (256 * VN) : 0;
+#define SM_SLICE_CASE(C)                                                                                         \
+  case C: {                                                                                                      \
+    const int nb = resident_blocks(pool_slices_kernel<T, C>, 256);                                               \
+    hipLaunchKernelGGL((pool_slices_kernel<T, C>), dim3(num_spans < nb ? num_spans : nb), dim3(256), 0, stream,  \
+                       G1, gidx, g_rows, span_offsets, num_spans, total_rows, Q, g_kv, beta_kv, eps, d, h, cout,  \
+                       err);                                                                                     \
+    return hipGetLastError();                                                                                    \
+  }
+  if (num_spans > 0) switch (cpl) {
+      SM_SLICE_CASE(1) SM_SLICE_CASE(2) SM_SLICE_CASE(3) SM_SLICE_CASE(4)
+      default:
+        break;
+    }
+#undef SM_SLICE_CASE
   const int nch = d % (64 * VN) == 0 ? d / (64 * VN) : 0;
 #define SM_POOL_CASE(C)                                                                                          \
   case C:                                                                                                        \
