@@ -900,40 +900,46 @@ __global__ __launch_bounds__(kPoolWaves * 64) void pool_rows_kernel(const T *__r
 // persistent workgroups of four waves, each taking spans blockIdx.x,
 // blockIdx.x + gridDim.x, ...  Wave w owns columns [w d/4, (w + 1) d/4);
 // lane l holds the 16-byte groups c * 64 + l (c < CPL) of that slice of
-// every row.  So the slice's score weights q_j g_j stay in registers for
-// the whole kernel, a span's rows (up to kPoolResident of them) stay in
-// registers from the scores to the weighted sum, and the only data crossing
-// waves are a few sums per row in LDS.
+// every row.  The slice's score weights q_j g_j, LN_kv gain and bias are
+// staged once per workgroup in LDS (each lane reads back only its own), and
+// the span's rows are read once: kPoolResident at a time into registers,
+// each group scored and folded into the weighted sum by an online softmax
+// before the next is loaded.  Only a few sums per row cross waves, through
+// LDS.
 //
 // With the shift K_rw = the slice's first element of row r, wave w forms
 //   S1 = sum (x - K),  S2 = sum (x - K)^2,  T_h = sum_{j in head h} q_j g_j (x_j - K)
-// over its slice.  The four slices' (S1, S2) combine by the pairwise
-// update of Chan, Golub and LeVeque into the row's mean mu_r and
+// over its slice.  The slices' (S1, S2) combine by the pairwise update of
+// Chan, Golub and LeVeque into the row's mean mu_r and
 // inv_r = 1 / sqrt(var_r + eps), and the score of head h is
-//   (inv_r sum_w [T_wh + (K_rw - mu_r) C_wh] + D_h) / sqrt(dh),
+//   s_rh = (inv_r sum_w [T_wh + (K_rw - mu_r) C_wh] + D_h) / sqrt(dh),
 //   C_wh = sum_{j in h, slice w} q_j g_j,  D_h = sum_{j in h} q_j beta_j,
-// i.e. q_h . LN_kv(x_r)_h / sqrt(dh).  With a_rh = alpha_rh inv_r (alpha the
-// per-head softmax over the span's rows) the pooled column j is
-//   g_j (sum_r a_rh (x_rj - K_rw) - E_wh) + beta_j,  E_wh = sum_r a_rh (mu_r - K_rw),
-// which is sum_r alpha_rh LN_kv(x_r)_j because each head's alphas sum to one.
-// The shifts keep the sums free of cancellation when a row's values sit
-// far from zero.
+// i.e. q_h . LN_kv(x_r)_h / sqrt(dh).  With p_rh = exp(s_rh - M_h) (M_h the
+// running maximum; earlier terms are rescaled when it moves), Z_h their
+// sum and a_rh = p_rh inv_r, the pooled column j is
+//   g_j (sum_r a_rh (x_rj - K_rw) - E_wh) / Z_h + beta_j,
+//   E_wh = sum_r a_rh (mu_r - K_rw),
+// which is sum_r alpha_rh LN_kv(x_r)_j for alpha = softmax_r(s_rh), since
+// each head's alphas sum to one.  The shifts keep the sums free of
+// cancellation when a row's values sit far from zero.
 constexpr int kPoolResident = 4;  // rows per group held in registers
 constexpr int kSliceHeads = 5;    // heads meeting one quarter of the columns (h <= 16, d/h a multiple of 64)
 
 template <typename T, int CPL>
-__global__ __launch_bounds__(256, 2) void pool_slices_kernel(const T *__restrict__ G1, const int32_t *__restrict__ gidx,
+__global__ __launch_bounds__(256, CPL <= 2 ? 3 : 2) void pool_slices_kernel(const T *__restrict__ G1, const int32_t *__restrict__ gidx,
                                                           int64_t g_rows, const int32_t *__restrict__ span_offsets,
                                                           int num_spans, int total_rows, const T *__restrict__ Q,
                                                           const T *__restrict__ g_kv, const T *__restrict__ beta_kv,
                                                           float eps, int d, int h, T *__restrict__ cout,
                                                           int32_t *err) {
-  constexpr int VN = Vec<T>::N;
-  __shared__ float sh_k[kMaxSpanLen][4], sh_s1[kMaxSpanLen][4], sh_s2[kMaxSpanLen][4];
-  __shared__ float sh_t[kMaxSpanLen][4][kSliceHeads];
-  __shared__ float sh_a[kMaxSpanLen][kMaxHeads];
-  __shared__ float sh_mu[kMaxSpanLen], sh_inv[kMaxSpanLen];
+  constexpr int VN = Vec<T>::N, R = kPoolResident;
+  __shared__ float sh_k[R][4], sh_s1[R][4], sh_s2[R][4];  // per row of the group and slice
+  __shared__ float sh_t[R][4][kSliceHeads];
+  __shared__ float sh_a[R][kMaxHeads], sh_mu[R];
+  __shared__ float sh_scale[kMaxHeads], sh_iz[kMaxHeads];
   __shared__ float sh_c[4][kSliceHeads], sh_dq[4][kSliceHeads];
+  __shared__ u32x4_t sh_gb[2][4 * 64 * CPL];        // g_kv, beta_kv as stored
+  __shared__ f32x4_t sh_wq[4 * 64 * CPL][VN / 4];   // q_j g_j
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int slice = d >> 2, dh = d / h;
   const int hf = (w * slice) / dh, nh = (w * slice + slice - 1) / dh - hf + 1;  // heads meeting this slice
@@ -942,7 +948,6 @@ __global__ __launch_bounds__(256, 2) void pool_slices_kernel(const T *__restrict
 #pragma unroll
   for (int c = 0; c < CPL; ++c) hd[c] = (c0 + c * 64 * VN) / dh - hf;
 
-  float wq[CPL][VN];  // q_j g_j
   {
     float cs[kSliceHeads], ds[kSliceHeads];
 #pragma unroll
@@ -950,17 +955,23 @@ __global__ __launch_bounds__(256, 2) void pool_slices_kernel(const T *__restrict
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       const int col = c0 + c * 64 * VN;
-      float qf[VN], gf[VN], bf[VN];
+      const u32x4_t gu = *(const u32x4_t *)(g_kv + col), bu = *(const u32x4_t *)(beta_kv + col);
+      sh_gb[0][(w * CPL + c) * 64 + lane] = gu;
+      sh_gb[1][(w * CPL + c) * 64 + lane] = bu;
+      float qf[VN], gf[VN], bf[VN], wq[VN];
       unpack_vec<T>(*(const u32x4_t *)(Q + col), qf);
-      unpack_vec<T>(*(const u32x4_t *)(g_kv + col), gf);
-      unpack_vec<T>(*(const u32x4_t *)(beta_kv + col), bf);
+      unpack_vec<T>(gu, gf);
+      unpack_vec<T>(bu, bf);
       float cc = 0.f, dd = 0.f;
 #pragma unroll
       for (int e = 0; e < VN; ++e) {
-        wq[c][e] = qf[e] * gf[e];
-        cc += wq[c][e];
+        wq[e] = qf[e] * gf[e];
+        cc += wq[e];
         dd += qf[e] * bf[e];
       }
+#pragma unroll
+      for (int v = 0; v < VN / 4; ++v)
+        sh_wq[(w * CPL + c) * 64 + lane][v] = f32x4_t{wq[4 * v], wq[4 * v + 1], wq[4 * v + 2], wq[4 * v + 3]};
 #pragma unroll
       for (int hs = 0; hs < kSliceHeads; ++hs)
         if (hd[c] == hs) {
@@ -980,9 +991,19 @@ __global__ __launch_bounds__(256, 2) void pool_slices_kernel(const T *__restrict
   }
   const float inv_sqrt_dh = 1.0f / sqrtf((float)dh), n_slice = (float)slice;
 
+  // the next span's row range is requested a span ahead
+  int nx0 = 0, nx1 = 0;
+  if ((int)blockIdx.x < num_spans) {
+    nx0 = span_offsets[blockIdx.x];
+    nx1 = span_offsets[blockIdx.x + 1];
+  }
   for (int s = blockIdx.x; s < num_spans; s += gridDim.x) {
     T *dst = cout + (int64_t)s * d;
-    const int r0 = span_offsets[s], r1 = span_offsets[s + 1];
+    const int r0 = nx0, r1 = nx1;
+    if (s + (int)gridDim.x < num_spans) {
+      nx0 = span_offsets[s + gridDim.x];
+      nx1 = span_offsets[s + gridDim.x + 1];
+    }
     const int n = r1 - r0;
     bool ok = n >= 1 && n <= kMaxSpanLen && r0 >= 0 && r1 <= total_rows;
     if (s == 0 && r0 != 0) ok = false;
@@ -993,39 +1014,48 @@ __global__ __launch_bounds__(256, 2) void pool_slices_kernel(const T *__restrict
       for (int c = 0; c < CPL; ++c) *(u32x4_t *)(dst + c0 + c * 64 * VN) = u32x4_t{0u, 0u, 0u, 0u};
       continue;
     }
-    auto load_group = [&](u32x4_t (&xr)[kPoolResident][CPL], int g0, int nr) {
+    float M = -INFINITY, Z = 0.f;  // (thread hh < h: head hh's running maximum and sum)
+    float E = 0.f;                 // (lane hs < nh: E of head hf + hs)
+    float acc[CPL][VN];
 #pragma unroll
-      for (int rr = 0; rr < kPoolResident; ++rr)
+    for (int c = 0; c < CPL; ++c)
+#pragma unroll
+      for (int e = 0; e < VN; ++e) acc[c][e] = 0.f;
+    for (int g0 = 0; g0 < n; g0 += R) {
+      const int nr = min(R, n - g0);
+      u32x4_t xr[R][CPL];
+#pragma unroll
+      for (int rr = 0; rr < R; ++rr)
         if (rr < nr) {
           const T *row = g1_row(G1, gidx, g_rows, r0 + g0 + rr, d, err) + c0;
 #pragma unroll
           for (int c = 0; c < CPL; ++c) xr[rr][c] = *(const u32x4_t *)(row + c * 64 * VN);
         }
-    };
-    // slice sums of every row
-    u32x4_t xr[kPoolResident][CPL];
-    for (int g0 = 0; g0 < n; g0 += kPoolResident) {
-      const int nr = min(kPoolResident, n - g0);
-      load_group(xr, g0, nr);
+      // slice sums of the group's rows
 #pragma unroll
-      for (int rr = 0; rr < kPoolResident; ++rr)
+      for (int rr = 0; rr < R; ++rr)
         if (rr < nr) {
-          const int r = g0 + rr;
           float xk[VN];
           unpack_vec<T>(xr[rr][0], xk);
           const float K = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(xk[0])));
           float s1 = 0.f, s2 = 0.f, tc[CPL];
 #pragma unroll
           for (int c = 0; c < CPL; ++c) {
-            float x[VN];
+            float x[VN], wq[VN];
             unpack_vec<T>(xr[rr][c], x);
+#pragma unroll
+            for (int v = 0; v < VN / 4; ++v) {
+              const f32x4_t q4 = sh_wq[(w * CPL + c) * 64 + lane][v];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) wq[4 * v + e] = q4[e];
+            }
             float t = 0.f;
 #pragma unroll
             for (int e = 0; e < VN; ++e) {
               const float dx = x[e] - K;
               s1 += dx;
               s2 = fmaf(dx, dx, s2);
-              t = fmaf(wq[c][e], dx, t);
+              t = fmaf(wq[e], dx, t);
             }
             tc[c] = t;
           }
@@ -1038,97 +1068,101 @@ __global__ __launch_bounds__(256, 2) void pool_slices_kernel(const T *__restrict
 #pragma unroll
               for (int c = 0; c < CPL; ++c) t += hd[c] == hs ? tc[c] : 0.f;
               t = wave_sum(t);
-              if (lane == 0) sh_t[r][w][hs] = t;
+              if (lane == 0) sh_t[rr][w][hs] = t;
             }
           if (lane == 0) {
-            sh_k[r][w] = K;
-            sh_s1[r][w] = s1;
-            sh_s2[r][w] = s2;
+            sh_k[rr][w] = K;
+            sh_s1[rr][w] = s1;
+            sh_s2[rr][w] = s2;
           }
+          __builtin_amdgcn_sched_barrier(0);  // one row at a time: bounds the live unpacked values
         }
-    }
-    lds_barrier();
-    // row statistics, scores and the per-head softmax: thread hh < h takes head hh
-    if (tid < h) {
-      const int hh = tid, wf = (hh * dh) / slice, wl = (hh * dh + dh - 1) / slice;
-      float m = -INFINITY;
-      for (int r = 0; r < n; ++r) {
-        float mw[4], mean = 0.f, m2 = 0.f;
+      lds_barrier();
+      // the group's row statistics and scores, folded into the running
+      // softmax: thread hh < h takes head hh
+      if (tid < h) {
+        const int hh = tid, wf = (hh * dh) / slice, wl = (hh * dh + dh - 1) / slice;
+        float sc[R], iv[R], gmax = -INFINITY;
 #pragma unroll
-        for (int ww = 0; ww < 4; ++ww) {
-          const float a1 = sh_s1[r][ww];
-          mw[ww] = sh_k[r][ww] + a1 / n_slice;
-          mean += mw[ww];
-          m2 += sh_s2[r][ww] - a1 * (a1 / n_slice);
-        }
-        mean *= 0.25f;
+        for (int rr = 0; rr < R; ++rr)
+          if (rr < nr) {
+            float mw[4], mean = 0.f, m2 = 0.f;
 #pragma unroll
-        for (int ww = 0; ww < 4; ++ww) m2 += n_slice * (mw[ww] - mean) * (mw[ww] - mean);
-        const float inv = 1.0f / sqrtf(fmaxf(m2, 0.f) / d + eps);
-        float t = 0.f, dq = 0.f;
-        for (int ww = wf; ww <= wl; ++ww) {
-          const int hs = hh - (ww * slice) / dh;
-          t += sh_t[r][ww][hs] + (sh_k[r][ww] - mean) * sh_c[ww][hs];
-          dq += sh_dq[ww][hs];
-        }
-        const float sc = (inv * t + dq) * inv_sqrt_dh;
-        sh_a[r][hh] = sc;
-        m = fmaxf(m, sc);
-        sh_mu[r] = mean;  // the same value from every head's thread
-        sh_inv[r] = inv;
+            for (int ww = 0; ww < 4; ++ww) {
+              const float a1 = sh_s1[rr][ww];
+              mw[ww] = sh_k[rr][ww] + a1 / n_slice;
+              mean += mw[ww];
+              m2 += sh_s2[rr][ww] - a1 * (a1 / n_slice);
+            }
+            mean *= 0.25f;
+#pragma unroll
+            for (int ww = 0; ww < 4; ++ww) m2 += n_slice * (mw[ww] - mean) * (mw[ww] - mean);
+            iv[rr] = 1.0f / sqrtf(fmaxf(m2, 0.f) / d + eps);
+            float t = 0.f, dq = 0.f;
+            for (int ww = wf; ww <= wl; ++ww) {
+              const int hs = hh - (ww * slice) / dh;
+              t += sh_t[rr][ww][hs] + (sh_k[rr][ww] - mean) * sh_c[ww][hs];
+              dq += sh_dq[ww][hs];
+            }
+            sc[rr] = (iv[rr] * t + dq) * inv_sqrt_dh;
+            gmax = fmaxf(gmax, sc[rr]);
+            if (hh == 0) sh_mu[rr] = mean;
+          }
+        const float Mn = fmaxf(M, gmax), scale = expf(M - Mn);  // 0 for the first group
+        Z *= scale;
+#pragma unroll
+        for (int rr = 0; rr < R; ++rr)
+          if (rr < nr) {
+            const float p = expf(sc[rr] - Mn);
+            Z += p;
+            sh_a[rr][hh] = p * iv[rr];
+          }
+        M = Mn;
+        sh_scale[hh] = scale;
+        if (g0 + R >= n) sh_iz[hh] = 1.0f / Z;
       }
-      float z = 0.f;
-      for (int r = 0; r < n; ++r) {
-        const float e = expf(sh_a[r][hh] - m);
-        sh_a[r][hh] = e;
-        z += e;
+      lds_barrier();
+      // fold the group into this wave's weighted sum (the rows are unpacked
+      // again: an empty asm on the packed registers keeps the compiler from
+      // holding the unpacked floats of the score pass across the barriers)
+#pragma unroll
+      for (int rr = 0; rr < R; ++rr)
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) asm volatile("" : "+v"(xr[rr][c]));
+      if (lane < nh) {
+        E *= sh_scale[hf + lane];
+        for (int rr = 0; rr < nr; ++rr) E += sh_a[rr][hf + lane] * (sh_mu[rr] - sh_k[rr][w]);
       }
-      const float iz = 1.0f / z;
-      for (int r = 0; r < n; ++r) sh_a[r][hh] = sh_a[r][hh] * iz * sh_inv[r];
-    }
-    lds_barrier();
-    // weighted sum over this wave's slice (the gain and bias are re-read,
-    // from cache, rather than held in registers across the span loop)
-    u32x4_t gp[CPL], bp[CPL];
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      gp[c] = *(const u32x4_t *)(g_kv + c0 + c * 64 * VN);
-      bp[c] = *(const u32x4_t *)(beta_kv + c0 + c * 64 * VN);
-    }
-    float E = 0.f;
-    if (lane < nh)
-      for (int r = 0; r < n; ++r) E += sh_a[r][hf + lane] * (sh_mu[r] - sh_k[r][w]);
-    float acc[CPL][VN];
+      for (int c = 0; c < CPL; ++c) {
+        const float sc = sh_scale[hf + hd[c]];
 #pragma unroll
-    for (int c = 0; c < CPL; ++c)
+        for (int e = 0; e < VN; ++e) acc[c][e] *= sc;
+      }
 #pragma unroll
-      for (int e = 0; e < VN; ++e) acc[c][e] = 0.f;
-    for (int g0 = 0; g0 < n; g0 += kPoolResident) {
-      const int nr = min(kPoolResident, n - g0);
-      if (n > kPoolResident) load_group(xr, g0, nr);  // else the rows are still held
-#pragma unroll
-      for (int rr = 0; rr < kPoolResident; ++rr)
+      for (int rr = 0; rr < R; ++rr)
         if (rr < nr) {
-          const int r = g0 + rr;
-          const float K = sh_k[r][w];
+          const float K = sh_k[rr][w];
 #pragma unroll
           for (int c = 0; c < CPL; ++c) {
-            const float a = sh_a[r][hf + hd[c]];
+            const float a = sh_a[rr][hf + hd[c]];
             float x[VN];
             unpack_vec<T>(xr[rr][c], x);
 #pragma unroll
             for (int e = 0; e < VN; ++e) acc[c][e] = fmaf(a, x[e] - K, acc[c][e]);
           }
         }
+      // (the next group's sums are written only after every wave has passed
+      // this group's second barrier, and read after its own first)
     }
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
-      const float ec = __shfl(E, hd[c]);
+      const float ec = __shfl(E, hd[c]), iz = sh_iz[hf + hd[c]];
       float gf[VN], bf[VN], y[VN];
-      unpack_vec<T>(gp[c], gf);
-      unpack_vec<T>(bp[c], bf);
+      unpack_vec<T>(sh_gb[0][(w * CPL + c) * 64 + lane], gf);
+      unpack_vec<T>(sh_gb[1][(w * CPL + c) * 64 + lane], bf);
 #pragma unroll
-      for (int e = 0; e < VN; ++e) y[e] = fmaf(gf[e], acc[c][e] - ec, bf[e]);
+      for (int e = 0; e < VN; ++e) y[e] = fmaf(gf[e], (acc[c][e] - ec) * iz, bf[e]);
       store_vec(dst + c0 + c * 64 * VN, y);
     }
   }
