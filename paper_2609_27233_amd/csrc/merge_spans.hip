@@ -209,7 +209,7 @@ template <typename OutT>
 __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
     const uint16_t *__restrict__ A, const int32_t *__restrict__ gather, int64_t a_rows,
     const uint16_t *__restrict__ B, const uint16_t *__restrict__ bias, OutT *__restrict__ C, int M, int N, int K,
-    int tiles_m, int tiles_n, int per_xcd, int32_t *err) {
+    int tiles_m, int tiles_n, int per_xcd, int staged, int32_t *err) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wm = w >> 2, wn = w & 3;  // this wave's 128 x 64 block of the tile
@@ -337,25 +337,80 @@ __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
 
   // 32x32 result layout (swapped): register 4 g + e of tile (i, j) holds
   // C[row 32 i + r32][col 32 j + 8 g + 4 h2 + e]
+  if (!staged) {  // straight from the MFMA layout (grids of a few waves of tiles)
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < 2; ++j) {
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int col = n0 + wn * 64 + j * 32 + 8 * g + 4 * h2;
-      const uint2 bb = *(const uint2 *)(bias + col);
-      const float b0 = __uint_as_float(bb.x << 16), b1 = __uint_as_float(bb.x & 0xffff0000u);
-      const float b2 = __uint_as_float(bb.y << 16), b3 = __uint_as_float(bb.y & 0xffff0000u);
+      for (int g = 0; g < 4; ++g) {
+        const int col = n0 + wn * 64 + j * 32 + 8 * g + 4 * h2;
+        const uint2 bb = *(const uint2 *)(bias + col);
+        const float b0 = __uint_as_float(bb.x << 16), b1 = __uint_as_float(bb.x & 0xffff0000u);
+        const float b2 = __uint_as_float(bb.y << 16), b3 = __uint_as_float(bb.y & 0xffff0000u);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = m0 + wm * 128 + i * 32 + r32;
-        if (row < M)
-          Store4<OutT>::put(C + (int64_t)row * N + col, gelu_erf(acc[i][j][4 * g + 0] + b0),
-                            gelu_erf(acc[i][j][4 * g + 1] + b1), gelu_erf(acc[i][j][4 * g + 2] + b2),
-                            gelu_erf(acc[i][j][4 * g + 3] + b3));
+        for (int i = 0; i < 4; ++i) {
+          const int row = m0 + wm * 128 + i * 32 + r32;
+          if (row < M)
+            Store4<OutT>::put(C + (int64_t)row * N + col, gelu_erf(acc[i][j][4 * g + 0] + b0),
+                              gelu_erf(acc[i][j][4 * g + 1] + b1), gelu_erf(acc[i][j][4 * g + 2] + b2),
+                              gelu_erf(acc[i][j][4 * g + 3] + b3));
+        }
       }
+    }
+    return;
+  }
+  // Epilogue through LDS, free once every wave is past the ring: the tile
+  // (bias and GELU applied, in OutT) goes row-major into LDS, HR rows at a
+  // time, with the 16-byte chunk c of row r at c ^ (r % CH); then the
+  // workgroup stores whole rows, 16 bytes per lane.  Stored straight from
+  // the MFMA layout, each lane's 8 or 16 bytes go to 32 rows per
+  // instruction, and the partial lines reach memory in pieces (4x the
+  // output's bytes written).  The swizzle makes the row reads free of bank
+  // conflicts.  Staging serialises the tile's last phase, so it pays when
+  // other workgroups' main loops overlap it: grids of many waves of tiles.
+  constexpr int CH = kLN * (int)sizeof(OutT) / 16;               // 16-byte chunks per tile row
+  constexpr int HR = kLLdsBytes / (kLN * (int)sizeof(OutT));     // tile rows per LDS pass
+  constexpr int EPC = 16 / (int)sizeof(OutT);                    // elements per chunk
+  __syncthreads();  // every wave's ring reads and loads are done
+#pragma unroll
+  for (int pass = 0; pass < kLM / HR; ++pass) {
+    if (pass > 0) __syncthreads();  // the previous pass's rows are stored
+    if (wm * 128 / HR == pass) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int lcol = wn * 64 + j * 32 + 8 * g + 4 * h2;
+          const uint2 bb = *(const uint2 *)(bias + n0 + lcol);
+          const float b0 = __uint_as_float(bb.x << 16), b1 = __uint_as_float(bb.x & 0xffff0000u);
+          const float b2 = __uint_as_float(bb.y << 16), b3 = __uint_as_float(bb.y & 0xffff0000u);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int lrow = wm * 128 + i * 32 + r32 - pass * HR;
+            const int c = lcol / EPC;
+            uint8_t *dstl = lds + lrow * (CH * 16) + ((c ^ (lrow & (CH - 1))) * 16) + (lcol % EPC) * (int)sizeof(OutT);
+            Store4<OutT>::put((OutT *)dstl, gelu_erf(acc[i][j][4 * g + 0] + b0), gelu_erf(acc[i][j][4 * g + 1] + b1),
+                              gelu_erf(acc[i][j][4 * g + 2] + b2), gelu_erf(acc[i][j][4 * g + 3] + b3));
+          }
+        }
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < HR * CH / kLThreads; ++k) {
+      const int q = tid + k * kLThreads, lrow = q / CH, c = q % CH;
+      const int row = m0 + pass * HR + lrow;
+      const u32x4_t v = *(const u32x4_t *)(lds + lrow * (CH * 16) + ((c ^ (lrow & (CH - 1))) * 16));
+      if (row < M) *(u32x4_t *)(C + (int64_t)row * N + n0 + c * EPC) = v;
     }
   }
 }
+
+// Output tiles from which the 256-tile GEMM stages a bf16 epilogue through
+// LDS (several waves of tiles, so that other workgroups' main loops overlap
+// it).  Measured: GEMM1 of the 70B-shaped batch (17,984 tiles) 19.6 -> 18.1
+// ms; at 1,856 tiles equal or faster; at 256 to 624 tiles, and for the fp32
+// output of the second projection at any size, slower or equal.
+constexpr int kStagedMinTiles = 1024;
 
 static bool use_gemm256(int M, int N, int K) {
   return N % kLN == 0 && K % (2 * kLK) == 0 && K >= 2 * kLK * kLStages &&
@@ -373,8 +428,9 @@ static hipError_t launch_gemm256(const uint16_t *A, const int32_t *gather, int64
   if (e != hipSuccess) return e;
   const int tiles_m = (M + kLM - 1) / kLM, tiles_n = N / kLN;
   const int per_xcd = (tiles_m * tiles_n + 7) / 8;
+  const int staged = sizeof(OutT) == 2 && tiles_m * tiles_n >= kStagedMinTiles;
   hipLaunchKernelGGL(gemm256_bf16_nt_gelu<OutT>, dim3(8 * per_xcd), dim3(kLThreads), kLLdsBytes, stream, A, gather,
-                     a_rows, B, bias, C, M, N, K, tiles_m, tiles_n, per_xcd, err);
+                     a_rows, B, bias, C, M, N, K, tiles_m, tiles_n, per_xcd, staged, err);
   return hipGetLastError();
 }
 
