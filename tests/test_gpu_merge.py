@@ -192,3 +192,55 @@ def test_merge_decode_time_batches(orc, d, S):
     e = rel_l2_max(out[torch.as_tensor(sample)].float().numpy(), ref)
     say("rel_l2_max", e)
     assert e <= TOL[torch.bfloat16]
+
+
+@pytest.mark.parametrize("d,h,lens", [
+    (2048, 8, [1, 4, 5, 9, 64, 255, 256, 2, 3, 8, 1, 17]),  # one to 64 groups of four rows
+    (6144, 6, [1, 2, 3, 4, 5, 6, 7, 13, 2, 4]),             # three groups per lane; heads straddle the quarters
+    (8192, 16, [4, 8, 1, 3, 12]),                             # four groups per lane, four heads per quarter
+])
+def test_merge_slice_pooling_spans_and_heads(orc, d, h, lens):
+    """The column-slice pooling kernel (d a multiple of 2048): spans from one
+    row to the 256-row limit, so the online softmax folds from one to 64
+    groups of rows, and head counts whose heads straddle the workgroup's
+    column quarters (d = 6144, h = 6: 1024-column heads over 1536-column
+    quarters)."""
+    rng = np.random.RandomState(d + h)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    vocab = 600
+    row_idx = rng.randint(0, vocab, size=int(offs[-1])).astype(np.int32)
+    g = wl.generator(d + 3 * h)
+    emb = wl.randn((vocab, d), torch.bfloat16, g, std=0.02)
+    params = wl.make_merge_params(d, h, torch.bfloat16, g, spread=True)
+    say("merge slice pooling", d, h, "spans", len(lens), "rows", int(offs[-1]))
+    out, err = _gpu_merge(emb.to(dev()), row_idx, offs, params, h, torch.bfloat16)
+    assert err == 0
+    ref = _oracle(orc, wl.to_f64(emb), row_idx, offs, params, h)
+    e = rel_l2_max(out.float().numpy(), ref)
+    say("rel_l2_max", e)
+    assert e <= TOL[torch.bfloat16]
+
+
+@pytest.mark.parametrize("d,h", [(1024, 4), (4096, 16)])
+def test_merge_slice_pooling_rows_far_from_zero_f32(orc, d, h):
+    """fp32 rows whose values sit far from zero (first-stage bias + 16, row
+    spread about 0.6): LN_kv statistics formed as E[x^2] - E[x]^2 would lose
+    about 2e-5 of relative precision here; the shifted sums of the slice
+    pooling keep the result within the fp32 bar (d = 1024 and 4096: one and
+    four 16-byte groups per lane)."""
+    rng = np.random.RandomState(d)
+    lens = rng.randint(1, 9, size=24)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    vocab = 300
+    row_idx = rng.randint(0, vocab, size=int(offs[-1])).astype(np.int32)
+    g = wl.generator(d + 11)
+    emb = wl.randn((vocab, d), torch.float32, g, std=1.0)
+    params = wl.make_merge_params(d, h, torch.float32, g, spread=True)
+    params["b_kv"] = params["b_kv"] + 16.0
+    say("merge f32 offset rows", d, h, "rows", int(offs[-1]))
+    out, err = _gpu_merge(emb.to(dev()), row_idx, offs, params, h, torch.float32)
+    assert err == 0
+    ref = _oracle(orc, wl.to_f64(emb), row_idx, offs, params, h)
+    e = rel_l2_max(out.numpy(), ref)
+    say("rel_l2_max", e)
+    assert e <= TOL[torch.float32]
