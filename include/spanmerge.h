@@ -174,7 +174,9 @@ size_t sm_merge_workspace_bytes(int total_rows, int num_spans, int d,
  *  ws, ws_bytes  workspace of at least sm_merge_workspace_bytes(...) bytes
  *  err           [1] device error word: EINVAL when a row index is outside
  *                [0, emb_rows) (that row is read as row 0) or the span
- *                offsets are not a valid CSR (those surrogates are zero)
+ *                offsets are not a valid CSR (the pooled vector of such a
+ *                span is zero, so its surrogate is LN_o(GELU(b_o)); the
+ *                other spans are pooled as usual)
  */
 sm_status sm_merge_spans(const void *emb, int64_t emb_rows,
                          const int32_t *row_idx, int total_rows,

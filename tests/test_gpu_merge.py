@@ -1,4 +1,6 @@
 """GPU merge_spans (M_phi) vs the oracle."""
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -244,3 +246,26 @@ def test_merge_slice_pooling_rows_far_from_zero_f32(orc, d, h):
     e = rel_l2_max(out.numpy(), ref)
     say("rel_l2_max", e)
     assert e <= TOL[torch.float32]
+
+
+@pytest.mark.parametrize("d", [256, 2048])
+def test_merge_empty_span_sets_einval(orc, d):
+    """A span with no rows (CSR offsets 0, 3, 3, 5): EINVAL, a zero pooled
+    vector for it (so its surrogate is LN_o(GELU(b_o))), and the other spans
+    still pooled as the oracle does (d = 256: the one-workgroup-per-span
+    kernel; d = 2048: the column-slice kernel)."""
+    g = wl.generator(d + 21)
+    emb = wl.randn((40, d), torch.bfloat16, g, std=0.02)
+    params = wl.make_merge_params(d, 4, torch.bfloat16, g, spread=True)
+    row_idx = np.array([3, 7, 11, 19, 23], np.int32)
+    say("merge empty span", d)
+    out, err = _gpu_merge(emb.to(dev()), row_idx, np.array([0, 3, 3, 5], np.int32), params, 4, torch.bfloat16)
+    assert err == sm.ERR_EINVAL
+    p64 = {k: wl.to_f64(v) for k, v in params.items()}
+    y = p64["b_o"] * 0.5 * (1.0 + np.vectorize(math.erf)(p64["b_o"] / math.sqrt(2.0)))
+    z_empty = (y - y.mean()) / np.sqrt(y.var() + 1e-5) * p64["g_o"] + p64["beta_o"]
+    ref = _oracle(orc, wl.to_f64(emb), row_idx, np.array([0, 3, 5], np.int32), params, 4)
+    ref = np.stack([ref[0], z_empty, ref[1]])
+    e = rel_l2_max(out.float().numpy(), ref)
+    say("rel_l2_max", e)
+    assert e <= TOL[torch.bfloat16]
