@@ -1,13 +1,13 @@
-"""Parity at the five workload configurations, at their full sizes.
+"""Parity at the five workloads, at their full sizes.
 
-Each test runs the configuration's job on the GPU and on the oracle in lock
+Each test runs the workload's job on the GPU and on the oracle in lock
 step: prompt compression (merge, pack, bulk append of the compressed
 prompt's K/V), then decode steps with decode-time merges (merge module,
 rollback of n-1 entries, append of the surrogate's K/V) or plain token
 appends, and decode attention after every step.  Integer state (block
 tables, lengths, free stack, pools) is compared bit for bit after every
 cache update; floating outputs are compared on every sequence for the small
-configurations and on a seeded sample of sequences / spans for the large
+workloads and on a seeded sample of sequences / spans for the large
 ones.
 """
 import numpy as np
@@ -178,8 +178,8 @@ def _decode_phase(orc, w, ls, emb, params, g, steps, max_len, attn_sample, check
             ls.attention(q, max_len, attn_sample)
 
 
-def test_config1_tiny_f32_full_chain(orc):
-    """Config 1: every output compared.  Prompt compression, the prompt K/V
+def test_tiny_f32_workload_full_chain(orc):
+    """The tiny fp32 workload (1 x 512 tokens, d = 256): every output compared.  Prompt compression, the prompt K/V
     from the test-only layer at compressed positions, then one decode-time
     merge (crop n-1, append the surrogate's K/V at its compressed position,
     attend with the surrogate's query) and one ordinary decode step."""
@@ -188,7 +188,7 @@ def test_config1_tiny_f32_full_chain(orc):
     g = wl.generator(w.seed)
     emb = wl.randn((w.vocab, w.d), torch.float32, g, std=0.02).to(dev())
     params = {k: v.to(dev()) for k, v in wl.make_merge_params(w.d, w.h, torch.float32, g).items()}
-    say("config 1: spans", len(P.span_len))
+    say("tiny fp32 workload: spans", len(P.span_len))
     z = _gpu_merge(emb, P.row_idx, P.span_offsets, params, w.h, torch.float32)
     _merge_check(orc, emb, params, w.h, P.row_idx, P.span_offsets, z, np.arange(len(P.span_len)), 1e-5)
     # oracle surrogates feed the test-only layer on both sides
@@ -250,7 +250,7 @@ def test_config1_tiny_f32_full_chain(orc):
 
 
 def _full_decode(orc, w, ls, emb, params, g, steps, max_len, pool_every, seqs_per_step):
-    """The configuration's whole decode run with the fused steps (the merge
+    """The workload's whole decode run with the fused steps (the merge
     steps crop, append and attend in one sm_decode_merge_step): every
     decode-time merge's spans all checked, integer state after every step,
     pools every `pool_every` steps, attention of every sequence at the first
@@ -280,8 +280,8 @@ def _full_decode(orc, w, ls, emb, params, g, steps, max_len, pool_every, seqs_pe
             say("step", s, "lengths", ls.oc.lengths[:4].tolist(), "worst attention rel_l2 so far", worst)
 
 
-def test_config2_prompt_compression_and_separate_decode_calls(orc):
-    """Config 2 at full size: all spans merged in one call (oracle on a
+def test_llama3_8b_batch_prompt_compression_and_separate_decode_calls(orc):
+    """The Llama-3-8B-shaped batch (16 x 4096-token prompts) at full size: all spans merged in one call (oracle on a
     sample), pack and bulk append bit-exact, then 9 decode steps through the
     separate append and attention calls, a decode-time merge at step 7.
     (The benchmark's own job, with the fused step for all 256 steps, is
@@ -292,7 +292,7 @@ def test_config2_prompt_compression_and_separate_decode_calls(orc):
     emb = wl.randn((w.vocab, w.d), w.torch_dtype, g, device="cuda", std=0.02)
     params = wl.make_merge_params(w.d, w.h, w.torch_dtype, g, device="cuda")
     S = len(P.span_len)
-    say("config 2", w.name, "spans", S, "rows", len(P.row_idx))
+    say(w.name, "spans", S, "rows", len(P.row_idx))
     rng = np.random.RandomState(2)
     merge_sample = np.unique(np.concatenate([[0, S - 1], rng.choice(S, 254, replace=False)]))
     L0 = w.prompt_len - int(round(w.target * w.prompt_len))
@@ -307,21 +307,23 @@ def test_config2_prompt_compression_and_separate_decode_calls(orc):
     _decode_phase(orc, w, ls, emb, params, gk, steps, max_len, attn_sample, check_every=4, merge_sample_size=4)
 
 
-@pytest.mark.parametrize("cid", [3, 5])
-def test_prompt_compression_and_full_decode(orc, cid):
-    """Configs 3 and 5 at full size for their whole runs: every prompt span
+@pytest.mark.parametrize("wid", [3, 5])
+def test_prompt_compression_and_full_decode(orc, wid):
+    """The long-context batch (4 x 32,768-token prompts, shuffled pages) and
+    the Llama-3-70B-shaped batch (32 x 8192) at full size for their whole runs: every prompt span
     merged in one call (1024 sampled spans plus the first and last checked),
     pack and bulk append bit-exact, then all decode steps (128 with a
-    decode-time merge every 8 steps for config 3, 64 for config 5) with the
+    decode-time merge every 8 steps for the long-context batch, 64 for the
+    70B-shaped one) with the
     fused step; at least 64 (sequence, head) rows checked per step."""
-    w = wl.WORKLOADS[cid]
+    w = wl.WORKLOADS[wid]
     P = wl.make_prompts(w)
     g = wl.generator(w.seed, "cuda")
     emb = wl.randn((w.vocab, w.d), w.torch_dtype, g, device="cuda", std=0.02)
     params = wl.make_merge_params(w.d, w.h, w.torch_dtype, g, device="cuda")
     S = len(P.span_len)
-    say("config", cid, w.name, "spans", S, "rows", len(P.row_idx))
-    rng = np.random.RandomState(cid)
+    say(w.name, "spans", S, "rows", len(P.row_idx))
+    rng = np.random.RandomState(wid)
     merge_sample = np.unique(np.concatenate([[0, S - 1], rng.choice(S, 1024, replace=False)]))
     L0 = w.prompt_len - int(round(w.target * w.prompt_len))
     steps = w.decode_steps
@@ -331,12 +333,12 @@ def test_prompt_compression_and_full_decode(orc, cid):
     ls = Lockstep(orc, w, NB, nb_seq, free_order=wl.free_order(NB, w.shuffled_pages, w.seed))
     gk = wl.generator(w.seed + 3)
     _prompt_phase(orc, w, ls, P, emb, params, gk, merge_sample)
-    _full_decode(orc, w, ls, emb, params, gk, steps, max_len, pool_every=32 if cid == 3 else 16,
+    _full_decode(orc, w, ls, emb, params, gk, steps, max_len, pool_every=32 if wid == 3 else 16,
                  seqs_per_step=-(-64 // w.num_q_heads))
 
 
-def test_config4_ragged_contexts_with_frequent_rollback(orc):
-    """Config 4: 128 sequences with contexts uniform in [512, 4096], all 256
+def test_qwen2_ragged_contexts_with_frequent_rollback(orc):
+    """The Qwen2-7B-shaped ragged batch: 128 sequences with contexts uniform in [512, 4096], all 256
     decode steps with the fused step, a decode-time merge (k ~ U{2,3,4},
     n = k + 1 tokens at d = 3584, all 128 spans checked) and crop every
     4 steps, attention over the ragged cache (3 sequences x 28 heads per
@@ -353,7 +355,7 @@ def test_config4_ragged_contexts_with_frequent_rollback(orc):
     ls = Lockstep(orc, w, NB, nb_seq)
     gk = wl.generator(w.seed + 3)
     offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
-    say("config 4 prefill rows", int(offs[-1]))
+    say("ragged batch prefill rows", int(offs[-1]))
     K = wl.randn((int(offs[-1]), w.num_kv_heads, w.head_dim), w.torch_dtype, gk)
     V = wl.randn((int(offs[-1]), w.num_kv_heads, w.head_dim), w.torch_dtype, gk)
     ls.append(np.arange(w.batch), offs, K, V)

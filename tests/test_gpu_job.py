@@ -31,7 +31,7 @@ def test_bench_job_all_256_steps_on_four_streams(orc):
     import bench
     w = wl.WORKLOADS[2]
     R, lanes = 4, 4
-    say("bench job: config 2, batches", R, "lanes", lanes)
+    say("bench job: 16 x 4096-token batches", R, "lanes", lanes)
     job = bench.Job(w, R, dev(), token_table=True, lanes=lanes)
     B, H, D, Hq = w.batch, w.num_kv_heads, w.head_dim, w.num_q_heads
     tol = TOL[torch.bfloat16]

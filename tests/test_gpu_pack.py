@@ -29,9 +29,9 @@ def _gpu_pack(P, emb=None, surrogates=None):
     return int(err.item()), pi.cpu().numpy()[:total], po.cpu().numpy(), ps.cpu().numpy(), packed
 
 
-@pytest.mark.parametrize("cid,B", [(1, 1), (2, 16), (3, 4), (5, 3)])
-def test_pack_indices_bit_exact(orc, cid, B):
-    w = wl.WORKLOADS[cid]
+@pytest.mark.parametrize("wid,B", [(1, 1), (2, 16), (3, 4), (5, 3)])
+def test_pack_indices_bit_exact(orc, wid, B):
+    w = wl.WORKLOADS[wid]
     P = wl.make_prompts(w, batch=B)
     say("pack", w.name, "B", B, "spans", len(P.span_len))
     st, res = orc.pack_spans(P.seq_offsets, P.span_start, P.span_len, P.seq_span_offsets)

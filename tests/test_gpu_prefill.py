@@ -114,7 +114,7 @@ def test_bad_requests_zero_their_rows_only(orc):
 
 
 def test_llama3_8b_prompt_batch_sampled(orc):
-    """The compressed config-2 prompt batch (16 x 2458 positions, 32/8 heads,
+    """The compressed Llama-3-8B-shaped prompt batch (16 x 2458 positions, 32/8 heads,
     head_dim 128) at full size, launched as the bench launches it.  Checked
     on the last 12 rows of every request and on the first 40 rows of two
     requests (the oracle runs those as requests of their own over the same
@@ -129,7 +129,7 @@ def test_llama3_8b_prompt_batch_sampled(orc):
     qo = np.arange(w.batch + 1, dtype=np.int32) * L0
     g = wl.generator(10)
     q = wl.randn((int(qo[-1]), Hq, D), torch.bfloat16, g)
-    say("prefill config-2 batch", w.batch, "x", L0)
+    say("prefill 8B-shaped batch", w.batch, "x", L0)
     out = _gpu_prefill(c, ids, qo, q, L0)
     assert c.error_bits() == 0
     k = 12
@@ -154,8 +154,8 @@ def test_llama3_8b_prompt_batch_sampled(orc):
 
 @pytest.mark.parametrize("wid", [3, 5])
 def test_prompt_batch_full_size_sampled(orc, wid):
-    """The compressed prompt batches of the long-context config (4 x 19661
-    positions over shuffled pages) and of the 70B-shaped config (32 x 4915
+    """The compressed prompt batches of the long-context batch (4 x 19661
+    positions over shuffled pages) and of the 70B-shaped batch (32 x 4915
     positions, 64 query heads, group 8) at full size; checked on the last 4
     rows of every request and the first 24 rows of one."""
     w = wl.WORKLOADS[wid]
@@ -169,7 +169,7 @@ def test_prompt_batch_full_size_sampled(orc, wid):
     gq = wl.generator(50 + wid, "cuda")
     q = wl.randn((int(qo[-1]), Hq, D), torch.bfloat16, gq, device="cuda")
     out = torch.full(q.shape, float("nan"), dtype=torch.bfloat16, device=dev())
-    say("prefill config", wid, w.batch, "x", L0)
+    say("prefill", w.name, w.batch, "x", L0)
     sm.prefill_attention(c, i32(ids), i32(qo), q, out, L0)
     torch.cuda.synchronize()
     assert c.error_bits() == 0

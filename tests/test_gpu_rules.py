@@ -109,8 +109,8 @@ def test_match_prompt_negative_ids_and_bad_offsets(orc):
     assert gs.tolist()[1] == gs.tolist()[2]                  # sequence 1 (5 > 3) got no spans
 
 
-def test_match_prompt_config2_batch(orc):
-    """The config-2 prompt batch (16 x 4096) with 2.17M synthetic rules of the
+def test_match_prompt_llama3_8b_batch(orc):
+    """The Llama-3-8B-shaped prompt batch (16 x 4096) with 2.17M synthetic rules of the
     Llama-3 rule counts, rules planted for a 40% reduction."""
     rules = wl.make_rules()
     toks, offs = wl.make_rule_prompts(rules, 16, 4096, 0.4, 128256, seed=3)
@@ -118,7 +118,7 @@ def test_match_prompt_config2_batch(orc):
     st, s0, ln, ru, sso = R.match_prompt(toks, offs)
     assert st == orc.OK
     t = _table(rules)
-    say("config-2 batch: spans", len(s0), "reduction", float((ln - 1).sum()) / len(toks))
+    say("8B-shaped batch: spans", len(s0), "reduction", float((ln - 1).sum()) / len(toks))
     g0, gl, gr, gs = _gpu_match(t, toks, offs)
     assert t.error_bits() == 0
     assert np.array_equal(gs, sso)
@@ -209,7 +209,7 @@ def test_match_decode_repeated_id_changes_nothing(orc):
 @pytest.mark.parametrize("B,T", [(4, 32768), (32, 8192)])
 def test_match_prompt_long_and_wide_batches(orc, B, T):
     """The prompt shapes of the long-context (4 x 32768: eight scan passes
-    per sequence) and 70B-shaped (32 x 8192) configs, 2.17M rules."""
+    per sequence) and 70B-shaped (32 x 8192) batches, 2.17M rules."""
     rules = wl.make_rules()
     toks, offs = wl.make_rule_prompts(rules, B, T, 0.4, 128256, seed=B)
     R = orc.OracleRules(rules)

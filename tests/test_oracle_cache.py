@@ -134,7 +134,7 @@ def test_failed_calls_change_nothing(orc):
 
 
 def test_rollback_and_surrogate_equals_prefill_with_surrogate(orc):
-    """Spec invariant 2 on the test-only layer: decode-time merge of the
+    """Merging equals prefilling the surrogate, on the test-only layer: a decode-time merge of the
     last n tokens (crop n-1 cached entries, append the surrogate's K/V at the
     compressed position) gives the cache of a prefill in which the span was
     replaced by the surrogate from the start; the surrogate's query then

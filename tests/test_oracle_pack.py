@@ -164,8 +164,8 @@ def test_rejects_invalid_spans(orc, spans):
 
 
 def test_generator_hits_targets():
-    for cid in (1, 2):
-        w = wl.WORKLOADS[cid]
+    for wid in (1, 2):
+        w = wl.WORKLOADS[wid]
         P = wl.make_prompts(w, batch=2)
         for b in range(2):
             lens = P.span_len[P.seq_span_offsets[b]:P.seq_span_offsets[b + 1]]
