@@ -111,13 +111,22 @@ def test_tabled_merge_llama3_8b_width(orc, S, nmin, nmax):
     assert e2 <= TOL[torch.bfloat16]
 
 
-def test_tabled_merge_bad_token_sets_einval():
-    d = 256
-    g = wl.generator(5)
-    emb = wl.randn((10, d), torch.bfloat16, g)
-    params = wl.make_merge_params(d, 4, torch.bfloat16, g)
-    say("tabled merge bad token")
+@pytest.mark.parametrize("d", [256, 2048])
+def test_tabled_merge_bad_token_sets_einval(orc, d):
+    """A token id past the table: EINVAL, that row read as row 0, the other
+    spans exact (d = 256: the one-workgroup-per-span pooling; d = 2048: the
+    column-slice pooling)."""
+    g = wl.generator(5 + d)
+    emb = wl.randn((10, d), torch.bfloat16, g, std=0.02)
+    params = wl.make_merge_params(d, 4, torch.bfloat16, g, spread=True)
+    say("tabled merge bad token", d)
     table = _table(emb.to(dev()), params, 4)
-    out, err = _tabled(table, np.array([1, 2, 10], np.int32), np.array([0, 2, 3], np.int32), params, 4)
+    out, err = _tabled(table, np.array([1, 2, 10, 4, 5], np.int32), np.array([0, 2, 3, 5], np.int32), params, 4)
     assert err == sm.ERR_EINVAL
     assert torch.isfinite(out.float()).all()
+    # the bad id is read as row 0, so span 1 pools row 0
+    ref = _oracle(orc, wl.to_f64(emb), np.array([1, 2, 0, 4, 5], np.int32), np.array([0, 2, 3, 5], np.int32),
+                  params, 4, np.arange(3))
+    e = rel_l2_max(out.float().numpy(), ref)
+    say("rel_l2_max", e)
+    assert e <= TOL[torch.bfloat16]
