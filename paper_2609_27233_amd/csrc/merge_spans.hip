@@ -145,39 +145,52 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_nt_gelu(const uint16_t *__re
 
 // ---------------------------------------------------------------------------
 // Large bf16 GEMM, same contract as above: 256x256 output tile per
-// workgroup, eight waves in a 2 x 4 grid (128 x 64 each) on
-// v_mfma_f32_32x32x16_bf16 (the 32x32 form sustains the full matrix-core
-// rate on gfx950; the 16x16x32 form measured about 64% of it).  K advances
-// 32 at a time through a ring of four LDS stages (4 x 32 KB) filled by
-// global_load_lds_dwordx4, which moves 16 bytes per lane from memory
-// straight into LDS without staging registers.  Waits are explicit
-// (s_waitcnt vmcnt + s_barrier) so that two k-tiles stay in flight behind
-// the one being consumed; each wave reads its next fragments while its
-// matrix cores work on the current ones, and the scheduler interleaves the
-// LDS reads and the ring refills with the MFMAs.
+// workgroup, four waves in a 2 x 2 grid (128 x 128 each, accumulators in
+// the accumulation registers, one wave per SIMD) on
+// v_mfma_f32_32x32x16_bf16.  K advances 64 at a time through two LDS
+// stages (2 x 64 KB) filled by global_load_lds_dwordx4, which moves 16
+// bytes per lane from memory straight into LDS without staging registers.
+// A 64-deep k-tile makes each operand row a 128-byte piece, so the L1 asks
+// the L2 for whole 128-byte lines (a 32-deep tile sends twice as many
+// 64-byte requests, and the L1 keeps only so many in flight).
 //
-// LDS layout of one operand stage: 256 rows x 64 bytes as 16-byte slots
-// row * 4 + (chunk ^ ((row >> 2) & 3)).  A 16-byte LDS read serves 16
+// One k-tile is four k steps of 16 MFMAs; each wave reads its next
+// fragments from LDS while its matrix core works on the current ones.
+// Before the last k step every wave waits for its own loads of the next
+// k-tile and for its fragment reads, then a barrier: after it the current
+// stage is held in registers by every wave (free) and the next k-tile is
+// in LDS.  The loads of the k-tile after next go into the free stage
+// spread over the last k step of this k-tile and the first two of the next
+// (about one every three MFMAs), so each has two to four k steps to land
+// and the CU's requests reach the L2 evenly rather than in one burst.  The
+// waits are explicit s_waitcnt and the instruction order is pinned by a
+// scheduling barrier after each MFMA.
+//
+// LDS layout of one operand stage: 256 rows x 128 bytes as 16-byte slots
+// row * 8 + (chunk ^ ((row >> 1) & 7)).  A 16-byte LDS read serves 16
 // lanes per cycle from 64 banks (256 bytes): the 16 lanes of a fragment
-// read take rows r .. r + 15 of one chunk, and the swizzle puts them in 16
-// distinct 16-byte bank groups (row % 4 picks the 64-byte quarter, the
-// swizzled chunk the slot within it), so the reads are free of bank
-// conflicts (SQ_LDS_BANK_CONFLICT = 0; a swizzle by (row >> 1) & 3 left
-// rows r and r + 8 in one group, 4 conflict cycles per read).  A
-// direct-to-LDS load writes 64 consecutive slots (one per lane), so lane l
-// of a load covers row base + l / 4, slot chunk l % 4, and fetches global
-// chunk (l % 4) ^ swizzle(row).
+// read take rows r .. r + 15 of one chunk; row parity picks the 128-byte
+// half of the bank row and the swizzled chunk the slot within it, so the
+// 16 reads hit 16 distinct bank groups.  A direct-to-LDS load writes 64
+// consecutive slots (one per lane): lane l of a load covers row
+// base + l / 8, slot l % 8, and fetches global chunk (l % 8) ^ swizzle(row).
 //
 // Tile order: the hardware hands workgroup b to XCD b % 8; XCD x takes the
 // logical tiles [x * per_xcd, (x + 1) * per_xcd) in groups of kGroupM row
 // tiles, so the 32 tiles in flight on one XCD share A rows and B columns
-// in its L2.
+// in its L2.  Each tile walks K from a rotated start: one k-tile per
+// column tile (the 8 column tiles in flight on an XCD are at most 8
+// k-tiles apart, so the A rows they share stay in L2) plus an eighth of K
+// per XCD, so that the eight XCDs do not ask for the same k offsets of
+// their rows, and of W, at the same time (measured 2.5-4% faster than all
+// tiles walking K from 0).  The sum over K of one output element thus
+// depends on its column tile and on the XCD its tile lands on.
 
-constexpr int kLM = 256, kLN = 256, kLK = 32, kLStages = 4, kLThreads = 512, kGroupM = 4;
+constexpr int kLM = 256, kLN = 256, kLK = 64, kLStages = 2, kLThreads = 256, kGroupM = 4;
 constexpr int kLStageBytes = kLM * kLK * 2;  // per operand
 constexpr int kLLdsBytes = 2 * kLStages * kLStageBytes;
 
-__device__ __forceinline__ int lds_swz(int row) { return (row >> 2) & 3; }
+__device__ __forceinline__ int lds_swz(int row) { return (row >> 1) & 7; }
 
 // s_waitcnt with vmcnt = N, lgkmcnt = 0, expcnt left open
 template <int N>
@@ -212,137 +225,147 @@ __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
     int tiles_m, int tiles_n, int per_xcd, int staged, int32_t *err) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w >> 2, wn = w & 3;  // this wave's 128 x 64 block of the tile
-  const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  const int wm = w >> 1, wn = w & 1;  // this wave's 128 x 128 block of the tile
+  const int xcd = blockIdx.x & 7;
+  const int t = xcd * per_xcd + (blockIdx.x >> 3);
   if (t >= tiles_m * tiles_n) return;
   const int gsz = kGroupM * tiles_n;
   const int g0 = (t / gsz) * kGroupM;
   const int gm = min(kGroupM, tiles_m - g0);
   const int tm = g0 + (t % gsz) % gm, tn = (t % gsz) / gm;
   const int m0 = tm * kLM, n0 = tn * kLN;
+  const int nk = K / kLK;
+  const int rot = (tn + xcd * (nk / 8)) % nk;  // first k-tile of this tile's walk
 
-  // sources of this lane's two loads per operand and stage (rows
-  // (u * 8 + w) * 16 + lane / 4); A rows past M re-read a valid row
-  const uint16_t *pa[2], *pb[2];
+  // Loads: per k-tile and operand, 32 direct-to-LDS loads of 1 KB (8 rows
+  // of 128 bytes); load u of wave w covers rows (4 u + w) * 8 + lane / 8.
+  // A rows past M re-read a valid row.
+  const uint16_t *pa[8];
+  const uint16_t *pb;
+  {
+    const int lrow = lane >> 3;
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int row = (u * 8 + w) * 16 + (lane >> 2);
-    const int chunk = (lane & 3) ^ lds_swz(row);
-    int64_t arow = m0 + row;
-    if (gather) {
-      int gi = (arow < M) ? gather[arow] : 0;
-      if (gi < 0 || gi >= a_rows) {
-        set_err(err, SM_ERR_EINVAL);
-        gi = 0;
+    for (int u = 0; u < 8; ++u) {
+      const int row = (4 * u + w) * 8 + lrow;
+      const int chunk = (lane & 7) ^ lds_swz(row);
+      int64_t arow = m0 + row;
+      if (gather) {
+        int gi = (arow < M) ? gather[arow] : 0;
+        if (gi < 0 || gi >= a_rows) {
+          set_err(err, SM_ERR_EINVAL);
+          gi = 0;
+        }
+        arow = gi;
+      } else if (arow >= M) {
+        arow = M - 1;
       }
-      arow = gi;
-    } else if (arow >= M) {
-      arow = M - 1;
+      pa[u] = A + arow * K + chunk * 8;
     }
-    pa[u] = A + arow * K + chunk * 8;
-    pb[u] = B + (int64_t)(n0 + row) * K + chunk * 8;
+    // the B rows of load u are those of load 0 plus 32 u (same swizzle)
+    const int row0 = w * 8 + lrow;
+    pb = B + (int64_t)(n0 + row0) * K + ((lane & 7) ^ lds_swz(row0)) * 8;
   }
+  const int64_t bstep = (int64_t)32 * K;
   uint8_t *sa = lds, *sb = lds + kLStages * kLStageBytes;
-  auto refill = [&](int kt, int stage) {  // k-tile kt into ring stage `stage`
-    const int ko = kt * kLK;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      load_to_lds16(pa[u] + ko, sa + stage * kLStageBytes + (u * 8 + w) * 1024);
-      load_to_lds16(pb[u] + ko, sb + stage * kLStageBytes + (u * 8 + w) * 1024);
-    }
+  auto load_q = [&](int kt, int stage, int q) {  // load q (A 0-7, B 8-15) of the kt-th k-tile of the walk
+    const int kr = kt + rot;
+    const int ko = (kr >= nk ? kr - nk : kr) * kLK;
+    const int u = q & 7;
+    if (q < 8) load_to_lds16(pa[u] + ko, sa + stage * kLStageBytes + (4 * u + w) * 1024);
+    else load_to_lds16(pb + u * bstep + ko, sb + stage * kLStageBytes + (4 * u + w) * 1024);
   };
 
   // 32x32x16 operands: lane l feeds row l % 32, k 8 (l / 32) .. +7 of a
-  // 16-wide k step, i.e. chunk 2 ks + l / 32 of the 64-byte row
+  // 16-deep k step ks, i.e. chunk 2 ks + l / 32 of the 128-byte row
   const int r32 = lane & 31, h2 = lane >> 5;
-  const int fo0 = (r32 * 4 + (h2 ^ lds_swz(r32))) * 16;
-  const int fo1 = (r32 * 4 + ((2 + h2) ^ lds_swz(r32))) * 16;
-  const int a_off = wm * 128 * 64, b_off = wn * 64 * 64;
+  int fo[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) fo[ks] = r32 * 128 + (((2 * ks + h2) ^ lds_swz(r32)) * 16);
+  const int a_off = wm * 128 * 128, b_off = wn * 128 * 128;
 
-  f32x16_t acc[4][2];
+  f32x16_t acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  // fa[4 ks + i]: rows 32 i of k step ks; fb[2 ks + j]: columns 32 j
-#define SM_READ_FRAGS(KT, FA, FB)                                                          \
-  {                                                                                        \
-    const uint8_t *la_ = sa + ((KT) & (kLStages - 1)) * kLStageBytes + a_off;              \
-    const uint8_t *lb_ = sb + ((KT) & (kLStages - 1)) * kLStageBytes + b_off;              \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                        \
-      FA[i] = *(const u32x4_t *)(la_ + i * 2048 + fo0);                                    \
-      FA[4 + i] = *(const u32x4_t *)(la_ + i * 2048 + fo1);                                \
-    }                                                                                      \
-    _Pragma("unroll") for (int j = 0; j < 2; ++j) {                                        \
-      FB[j] = *(const u32x4_t *)(lb_ + j * 2048 + fo0);                                    \
-      FB[2 + j] = *(const u32x4_t *)(lb_ + j * 2048 + fo1);                                \
-    }                                                                                      \
-  }
-  // Ring: k-tile t lives in stage t % 4.  The step that multiplies k-tile kt
-  // waits for kt + 1, passes the barrier (after which no wave still reads
-  // the stage of kt), refills that stage with k-tile kt + 4 and reads the
-  // fragments of kt + 1.  Past the end the last k-tile is loaded again
-  // (never read) so that the in-flight count, and thus every wait, is the
-  // same at each step.  Requires K % 64 == 0 and K >= 256.
-  const int nk = K / kLK;
+  // k-tile 0 in stage 0; the first 6 loads of k-tile 1 (the rest are
+  // issued during k steps 0 and 1 of k-tile 0)
+  u32x4_t fa0[4], fb0[4], fa1[4], fb1[4];
 #pragma unroll
-  for (int st = 0; st < kLStages; ++st) refill(st, st);
-  u32x4_t f0a[8], f0b[4], f1a[8], f1b[4];
-  wait_vmcnt_lgkm0<4 * (kLStages - 1)>();
+  for (int q = 0; q < 16; ++q) load_q(0, 0, q);
+#pragma unroll
+  for (int q = 0; q < 6; ++q) load_q(1, 1, q);
+  wait_vmcnt_lgkm0<6>();
   __builtin_amdgcn_s_barrier();
-  SM_READ_FRAGS(0, f0a, f0b);
-  auto refill_q = [&](int kt, int stage, int q) {  // load q (A, B, A, B) of refill(kt, stage)
-    const int ko = kt * kLK, u = q >> 1;
-    if (q & 1) load_to_lds16(pb[u] + ko, sb + stage * kLStageBytes + (u * 8 + w) * 1024);
-    else load_to_lds16(pa[u] + ko, sa + stage * kLStageBytes + (u * 8 + w) * 1024);
-  };
-  // One step on k-tile KT, whose fragments are in FA / FB: 16 MFMAs, each
-  // followed by one of the 12 fragment reads of k-tile KT + 1 (into GA / GB)
-  // and one of the 4 ring loads, in this fixed order (a scheduling barrier
-  // after each group).  The MFMAs go k step by k step over the 8
-  // accumulators, so two MFMAs into one accumulator are 8 apart; left to
-  // itself the scheduler put some of them back to back.  Swapped operands:
-  // the MFMA computes D[n][m], so a lane ends up holding four consecutive
-  // output columns of one row.
-#define SM_STEP(KT, FA, FB, GA, GB)                                                                  \
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    fa0[i] = *(const u32x4_t *)(sa + a_off + i * 4096 + fo[0]);
+    fb0[i] = *(const u32x4_t *)(sb + b_off + i * 4096 + fo[0]);
+  }
+
+  // One k step KS of the k-tile kt in stage ST, fragments in FA / FB: 16
+  // MFMAs over the 4 x 4 accumulators; after MFMA g < 8 one of the 8
+  // fragment reads of the next k step (of the next k-tile after k step 3,
+  // from the other stage) into GA / GB; after every third MFMA one load:
+  // k steps 0 and 1 issue loads 6-15 of k-tile kt + 1, k step 3 loads 0-5
+  // of k-tile kt + 2.  Past the end of K the last k-tile is loaded again
+  // (never read), so that every wait counts the same loads.
+#define SM_KSTEP(ST, KS, FA, FB, GA, GB)                                                             \
   {                                                                                                  \
-    wait_vmcnt_lgkm0<4 * (kLStages - 2)>();                                                          \
-    __builtin_amdgcn_s_barrier();                                                                    \
-    __builtin_amdgcn_sched_barrier(0);                                                               \
-    const int rk_ = min((KT) + kLStages, nk - 1), rs_ = (KT) & (kLStages - 1);                        \
-    const uint8_t *la_ = sa + (((KT) + 1) & (kLStages - 1)) * kLStageBytes + a_off;                  \
-    const uint8_t *lb_ = sb + (((KT) + 1) & (kLStages - 1)) * kLStageBytes + b_off;                  \
+    constexpr bool last_ = (KS) == 3;                                                                \
+    const int nst_ = last_ ? ((ST) ^ 1) : (ST);                                                      \
+    const int kn1_ = min(kt + 1, nk - 1), kn2_ = min(kt + 2, nk - 1);                                \
+    const uint8_t *la_ = sa + nst_ * kLStageBytes + a_off + fo[last_ ? 0 : ((KS) + 1) & 3];          \
+    const uint8_t *lb_ = sb + nst_ * kLStageBytes + b_off + fo[last_ ? 0 : ((KS) + 1) & 3];          \
     _Pragma("unroll") for (int g = 0; g < 16; ++g) {                                                 \
-      const int ks = g >> 3, i = (g >> 1) & 3, j = g & 1;                                            \
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(FB[2 * ks + j]),                 \
-                                                          as_bf16x8(FA[4 * ks + i]), acc[i][j], 0, 0, 0); \
-      if (g < 8)                                                                                     \
-        GA[g] = *(const u32x4_t *)(la_ + (g & 3) * 2048 + ((g >> 2) ? fo1 : fo0));                   \
-      else if (g < 12)                                                                               \
-        GB[g - 8] = *(const u32x4_t *)(lb_ + ((g - 8) & 1) * 2048 + (((g - 8) >> 1) ? fo1 : fo0));   \
-      if (g < 4) refill_q(rk_, rs_, g);                                                              \
+      const int i = g >> 2, j = g & 3;                                                               \
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(FB[j]), as_bf16x8(FA[i]), acc[i][j], \
+                                                          0, 0, 0);                                  \
+      if (g < 8) {                                                                                   \
+        if (g & 1) GB[g >> 1] = *(const u32x4_t *)(lb_ + (g >> 1) * 4096);                           \
+        else GA[g >> 1] = *(const u32x4_t *)(la_ + (g >> 1) * 4096);                                 \
+      }                                                                                              \
+      if (g % 3 == 0) {                                                                              \
+        const int q_ = g / 3;                                                                        \
+        if (last_) load_q(kn2_, (ST), q_);                                                           \
+        else if ((KS) == 0 && q_ < 5) load_q(kn1_, (ST) ^ 1, 6 + q_);                                \
+        else if ((KS) == 1 && q_ < 5) load_q(kn1_, (ST) ^ 1, 11 + q_);                               \
+      }                                                                                              \
       __builtin_amdgcn_sched_barrier(0);                                                             \
     }                                                                                                \
   }
-  for (int kt = 0; kt < nk; kt += 2) {
-    SM_STEP(kt, f0a, f0b, f1a, f1b);
-    SM_STEP(kt + 1, f1a, f1b, f0a, f0b);  // past the end: reads a stale stage, unused
+  // A k-tile: k steps 0-2; wait for this wave's loads of the next k-tile
+  // and its fragment reads, barrier; k step 3.
+#define SM_KTILE(ST)                                                                                 \
+  {                                                                                                  \
+    SM_KSTEP(ST, 0, fa0, fb0, fa1, fb1);                                                             \
+    SM_KSTEP(ST, 1, fa1, fb1, fa0, fb0);                                                             \
+    SM_KSTEP(ST, 2, fa0, fb0, fa1, fb1);                                                             \
+    wait_vmcnt_lgkm0<0>();                                                                           \
+    __builtin_amdgcn_s_barrier();                                                                    \
+    __builtin_amdgcn_sched_barrier(0);                                                               \
+    SM_KSTEP(ST, 3, fa1, fb1, fa0, fb0);                                                             \
   }
-#undef SM_STEP
+  for (int kt = 0; kt < nk; ++kt) {  // nk is even: stage 0, then stage 1
+    SM_KTILE(0);
+    ++kt;
+    SM_KTILE(1);
+  }
+#undef SM_KTILE
+#undef SM_KSTEP
   wait_vmcnt_lgkm0<0>();
-#undef SM_READ_FRAGS
 
   // 32x32 result layout (swapped): register 4 g + e of tile (i, j) holds
   // C[row 32 i + r32][col 32 j + 8 g + 4 h2 + e]
   if (!staged) {  // straight from the MFMA layout (grids of a few waves of tiles)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < 4; ++j) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int col = n0 + wn * 64 + j * 32 + 8 * g + 4 * h2;
+        const int col = n0 + wn * 128 + j * 32 + 8 * g + 4 * h2;
         const uint2 bb = *(const uint2 *)(bias + col);
         const float b0 = __uint_as_float(bb.x << 16), b1 = __uint_as_float(bb.x & 0xffff0000u);
         const float b2 = __uint_as_float(bb.y << 16), b3 = __uint_as_float(bb.y & 0xffff0000u);
@@ -376,10 +399,10 @@ __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
     if (pass > 0) __syncthreads();  // the previous pass's rows are stored
     if (wm * 128 / HR == pass) {
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
+      for (int j = 0; j < 4; ++j) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int lcol = wn * 64 + j * 32 + 8 * g + 4 * h2;
+          const int lcol = wn * 128 + j * 32 + 8 * g + 4 * h2;
           const uint2 bb = *(const uint2 *)(bias + n0 + lcol);
           const float b0 = __uint_as_float(bb.x << 16), b1 = __uint_as_float(bb.x & 0xffff0000u);
           const float b2 = __uint_as_float(bb.y << 16), b3 = __uint_as_float(bb.y & 0xffff0000u);
@@ -395,7 +418,7 @@ __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
       }
     }
     __syncthreads();
-#pragma unroll
+#pragma unroll 8
     for (int k = 0; k < HR * CH / kLThreads; ++k) {
       const int q = tid + k * kLThreads, lrow = q / CH, c = q % CH;
       const int row = m0 + pass * HR + lrow;
