@@ -829,6 +829,15 @@ def merge_70b_report(sm, L, dev, stream, reps=3):
     flop_t = 2.0 * w5.d * w5.d * S5
     agree = float((z5t.float() - z5.float()).norm(dim=1).div(z5.float().norm(dim=1)).max())
     del table5
+    # context, not part of the path: the library GEMM (torch.nn.functional.linear,
+    # hipBLASLt on ROCm) on the first projection's plain product over the
+    # same rows, gathered beforehand (no gather, bias or GELU in the timed call)
+    with torch.cuda.stream(stream):
+        ag = emb5.index_select(0, ri.long())
+        w_kv = par5["W_kv"]
+        t_lib = _time(lambda: torch.nn.functional.linear(ag, w_kv), stream, reps)
+    del ag
+    flop_lib = 2.0 * w5.d * w5.d * R5
     return {
         "spans": S5, "rows": R5, "d": w5.d, "ms": round(t5, 3),
         "TFLOPs": round(flop5 / (t5 * 1e-3) / 1e12, 1),
@@ -841,6 +850,10 @@ def merge_70b_report(sm, L, dev, stream, reps=3):
             "max_rel_l2_vs_direct": round(agree, 5),
             "note": "sm_merge_token_table over the 128256-row vocabulary, once; sm_merge_spans_tabled over the "
                     "same spans reads the first stage by token id"},
+        "library_gemm_reference": {
+            "ms": round(t_lib, 3), "TFLOPs": round(flop_lib / (t_lib * 1e-3) / 1e12, 1),
+            "note": "context only: torch.nn.functional.linear (hipBLASLt) on the first projection's plain product, rows gathered "
+                    "beforehand, no bias or GELU"},
         "note": "one sm_merge_spans call over every span of the 32 x 8192 prompts; FLOP = 2 d^2 (rows + spans) "
                 "for the two projections (pooling and LayerNorm are O(d) per row)"}
 
