@@ -154,17 +154,16 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_nt_gelu(const uint16_t *__re
 // the L2 for whole 128-byte lines (a 32-deep tile sends twice as many
 // 64-byte requests, and the L1 keeps only so many in flight).
 //
-// One k-tile is four k steps of 16 MFMAs; each wave reads its next
-// fragments from LDS while its matrix core works on the current ones.
-// Before the last k step every wave waits for its own loads of the next
-// k-tile and for its fragment reads, then a barrier: after it the current
-// stage is held in registers by every wave (free) and the next k-tile is
-// in LDS.  The loads of the k-tile after next go into the free stage
-// spread over the last k step of this k-tile and the first two of the next
-// (about one every three MFMAs), so each has two to four k steps to land
-// and the CU's requests reach the L2 evenly rather than in one burst.  The
-// waits are explicit s_waitcnt and the instruction order is pinned by a
-// scheduling barrier after each MFMA.
+// One k-tile is four k steps of 16 MFMAs.  Each wave holds a whole k-tile
+// of fragments in registers (128 VGPRs): during k step 0 it reads those of
+// k steps 1-3, then waits for them and passes a barrier, after which the
+// stage is free; k steps 1 and 2 load the k-tile after next into it (one
+// load every other MFMA, so the CU's requests reach the L2 evenly); before
+// k step 3 each wave waits for its own loads of the next k-tile and passes
+// a second barrier, and k step 3 reads the next k-tile's first fragments.
+// Each load thus has five to six k steps to land.  The waits are explicit
+// s_waitcnt and the instruction order is pinned by a scheduling barrier
+// after each MFMA.
 //
 // LDS layout of one operand stage: 256 rows x 128 bytes as 16-byte slots
 // row * 8 + (chunk ^ ((row >> 1) & 7)).  A 16-byte LDS read serves 16
@@ -291,63 +290,69 @@ __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  // k-tile 0 in stage 0; the first 6 loads of k-tile 1 (the rest are
-  // issued during k steps 0 and 1 of k-tile 0)
-  u32x4_t fa0[4], fb0[4], fa1[4], fb1[4];
+  // k-tiles 0 and 1 in stages 0 and 1; the fragments of k step 0
+  u32x4_t fa[4][4], fb[4][4];  // [k step][32-row block]
 #pragma unroll
   for (int q = 0; q < 16; ++q) load_q(0, 0, q);
 #pragma unroll
-  for (int q = 0; q < 6; ++q) load_q(1, 1, q);
-  wait_vmcnt_lgkm0<6>();
+  for (int q = 0; q < 16; ++q) load_q(1, 1, q);
+  wait_vmcnt_lgkm0<16>();
   __builtin_amdgcn_s_barrier();
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    fa0[i] = *(const u32x4_t *)(sa + a_off + i * 4096 + fo[0]);
-    fb0[i] = *(const u32x4_t *)(sb + b_off + i * 4096 + fo[0]);
+    fa[0][i] = *(const u32x4_t *)(sa + a_off + i * 4096 + fo[0]);
+    fb[0][i] = *(const u32x4_t *)(sb + b_off + i * 4096 + fo[0]);
   }
 
-  // One k step KS of the k-tile kt in stage ST, fragments in FA / FB: 16
-  // MFMAs over the 4 x 4 accumulators; after MFMA g < 8 one of the 8
-  // fragment reads of the next k step (of the next k-tile after k step 3,
-  // from the other stage) into GA / GB; after every third MFMA one load:
-  // k steps 0 and 1 issue loads 6-15 of k-tile kt + 1, k step 3 loads 0-5
-  // of k-tile kt + 2.  Past the end of K the last k-tile is loaded again
-  // (never read), so that every wait counts the same loads.
-#define SM_KSTEP(ST, KS, FA, FB, GA, GB)                                                             \
+  // One k step KS of the k-tile kt in stage ST: 16 MFMAs over the 4 x 4
+  // accumulators, each followed by
+  //  * k step 0: two of the 24 fragment reads of k steps 1-3 (after MFMAs
+  //    0-11);
+  //  * k steps 1 and 2: every other MFMA, one of the 16 loads of k-tile
+  //    kt + 2 into this (by then free) stage; past the end of K the last
+  //    k-tile is loaded again (never read), so that every wait counts the
+  //    same loads;
+  //  * k step 3: one of the 8 fragment reads of k step 0 of k-tile kt + 1
+  //    (after MFMAs 0-7), from the other stage.
+#define SM_KSTEP(ST, KS)                                                                             \
   {                                                                                                  \
-    constexpr bool last_ = (KS) == 3;                                                                \
-    const int nst_ = last_ ? ((ST) ^ 1) : (ST);                                                      \
-    const int kn1_ = min(kt + 1, nk - 1), kn2_ = min(kt + 2, nk - 1);                                \
-    const uint8_t *la_ = sa + nst_ * kLStageBytes + a_off + fo[last_ ? 0 : ((KS) + 1) & 3];          \
-    const uint8_t *lb_ = sb + nst_ * kLStageBytes + b_off + fo[last_ ? 0 : ((KS) + 1) & 3];          \
+    const int kn2_ = min(kt + 2, nk - 1);                                                            \
     _Pragma("unroll") for (int g = 0; g < 16; ++g) {                                                 \
       const int i = g >> 2, j = g & 3;                                                               \
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(FB[j]), as_bf16x8(FA[i]), acc[i][j], \
-                                                          0, 0, 0);                                  \
-      if (g < 8) {                                                                                   \
-        if (g & 1) GB[g >> 1] = *(const u32x4_t *)(lb_ + (g >> 1) * 4096);                           \
-        else GA[g >> 1] = *(const u32x4_t *)(la_ + (g >> 1) * 4096);                                 \
-      }                                                                                              \
-      if (g % 3 == 0) {                                                                              \
-        const int q_ = g / 3;                                                                        \
-        if (last_) load_q(kn2_, (ST), q_);                                                           \
-        else if ((KS) == 0 && q_ < 5) load_q(kn1_, (ST) ^ 1, 6 + q_);                                \
-        else if ((KS) == 1 && q_ < 5) load_q(kn1_, (ST) ^ 1, 11 + q_);                               \
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fb[KS][j]), as_bf16x8(fa[KS][i]), \
+                                                          acc[i][j], 0, 0, 0);                       \
+      if ((KS) == 0) {                                                                               \
+        if (g < 12) {                                                                                \
+          const int rk_ = 1 + g / 4, rq_ = g & 3;                                                    \
+          fa[rk_][rq_] = *(const u32x4_t *)(sa + (ST) * kLStageBytes + a_off + fo[rk_] + rq_ * 4096); \
+          fb[rk_][rq_] = *(const u32x4_t *)(sb + (ST) * kLStageBytes + b_off + fo[rk_] + rq_ * 4096); \
+        }                                                                                            \
+      } else if ((KS) == 1 || (KS) == 2) {                                                           \
+        if ((g & 1) == 0) load_q(kn2_, (ST), ((KS) - 1) * 8 + (g >> 1));                             \
+      } else if (g < 8) {                                                                            \
+        const int o_ = ((ST) ^ 1) * kLStageBytes + fo[0] + (g >> 1) * 4096;                          \
+        if (g & 1) fb[0][g >> 1] = *(const u32x4_t *)(sb + b_off + o_);                              \
+        else fa[0][g >> 1] = *(const u32x4_t *)(sa + a_off + o_);                                    \
       }                                                                                              \
       __builtin_amdgcn_sched_barrier(0);                                                             \
     }                                                                                                \
   }
-  // A k-tile: k steps 0-2; wait for this wave's loads of the next k-tile
-  // and its fragment reads, barrier; k step 3.
+  // A k-tile: k step 0; this wave's fragment reads done, barrier (the stage
+  // is free: every wave holds the k-tile in registers); k steps 1 and 2;
+  // this wave's loads of k-tile kt + 1 done (those of kt + 2 may still be
+  // in flight), barrier (k-tile kt + 1 is in LDS); k step 3.
 #define SM_KTILE(ST)                                                                                 \
   {                                                                                                  \
-    SM_KSTEP(ST, 0, fa0, fb0, fa1, fb1);                                                             \
-    SM_KSTEP(ST, 1, fa1, fb1, fa0, fb0);                                                             \
-    SM_KSTEP(ST, 2, fa0, fb0, fa1, fb1);                                                             \
-    wait_vmcnt_lgkm0<0>();                                                                           \
+    SM_KSTEP(ST, 0);                                                                                 \
+    wait_vmcnt_lgkm0<16>();                                                                          \
     __builtin_amdgcn_s_barrier();                                                                    \
     __builtin_amdgcn_sched_barrier(0);                                                               \
-    SM_KSTEP(ST, 3, fa1, fb1, fa0, fb0);                                                             \
+    SM_KSTEP(ST, 1);                                                                                 \
+    SM_KSTEP(ST, 2);                                                                                 \
+    wait_vmcnt_lgkm0<16>();                                                                          \
+    __builtin_amdgcn_s_barrier();                                                                    \
+    __builtin_amdgcn_sched_barrier(0);                                                               \
+    SM_KSTEP(ST, 3);                                                                                 \
   }
   for (int kt = 0; kt < nk; ++kt) {  // nk is even: stage 0, then stage 1
     SM_KTILE(0);
