@@ -1373,11 +1373,151 @@ using namespace sm;
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+
+// ---------------------------------------------------------------------------
+// Row order of a large first stage.  The gathered rows are token ids in span
+// order, scattered over the embedding table, and the 256-tile GEMM reads
+// each of a tile's 256 rows once per 64-deep k-tile: rows from all over the
+// table cost address translations and DRAM pages at every k-tile, and a
+// repeated token is fetched by as many tiles as it has occurrences.  A
+// stable counting sort of the rows by token-id bucket (kSortBuckets
+// buckets of consecutive ids) puts nearby and repeated ids in the same
+// tiles.  The GEMM then writes G1 in sorted order, and the pooling kernel
+// reads CSR row r as G1 row inv[r].  Three launches: per-chunk bucket
+// counts, their exclusive scan in (bucket, chunk) order, and a per-chunk
+// scatter that keeps the rows of one bucket in their CSR order, so the
+// permutation is the same on every run.
+constexpr int kSortBuckets = 4096, kSortChunk = 4096;
+
+__device__ __forceinline__ int sort_bucket(int32_t t, int64_t vocab) {
+  if (t < 0) return 0;
+  if (t >= vocab) return kSortBuckets - 1;  // (the GEMM flags the id)
+  return (int)((int64_t)t * kSortBuckets / vocab);
+}
+
+// grid: one workgroup of 256 per chunk of kSortChunk rows
+__global__ __launch_bounds__(256) void sort_count_kernel(const int32_t *__restrict__ tok, int n, int64_t vocab,
+                                                         int32_t *__restrict__ hist) {
+  __shared__ int h[kSortBuckets];
+  for (int i = threadIdx.x; i < kSortBuckets; i += 256) h[i] = 0;
+  __syncthreads();
+  const int r0 = blockIdx.x * kSortChunk, r1 = min(n, r0 + kSortChunk);
+  for (int r = r0 + (int)threadIdx.x; r < r1; r += 256) atomicAdd(&h[sort_bucket(tok[r], vocab)], 1);
+  __syncthreads();
+  for (int i = threadIdx.x; i < kSortBuckets; i += 256) hist[(int64_t)blockIdx.x * kSortBuckets + i] = h[i];
+}
+
+// one workgroup of 1024: hist[c][b] becomes the first sorted position of
+// chunk c's rows in bucket b (buckets in order, chunks in order within one)
+__global__ __launch_bounds__(1024) void sort_scan_kernel(int32_t *__restrict__ hist, int nchunks) {
+  __shared__ int red[16];
+  constexpr int BPT = kSortBuckets / 1024;  // buckets per thread
+  const int b0 = threadIdx.x * BPT;
+  static_assert(BPT == 4, "one 16-byte group of buckets per thread");
+  // (the chunks are taken 8 at a time, so that 8 loads are in flight)
+  int tot[BPT] = {0, 0, 0, 0}, sum = 0;
+  for (int c0 = 0; c0 < nchunks; c0 += 8) {
+    int4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      v[u] = c0 + u < nchunks ? *(const int4 *)&hist[(int64_t)(c0 + u) * kSortBuckets + b0] : make_int4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      tot[0] += v[u].x;
+      tot[1] += v[u].y;
+      tot[2] += v[u].z;
+      tot[3] += v[u].w;
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < BPT; ++k) sum += tot[k];
+  int total;
+  const int base = block_inclusive_scan(sum, red, &total) - sum;
+  int run[BPT];
+  run[0] = base;
+#pragma unroll
+  for (int k = 1; k < BPT; ++k) run[k] = run[k - 1] + tot[k - 1];
+  for (int c0 = 0; c0 < nchunks; c0 += 8) {
+    int4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      v[u] = c0 + u < nchunks ? *(const int4 *)&hist[(int64_t)(c0 + u) * kSortBuckets + b0] : make_int4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (c0 + u < nchunks) {
+        *(int4 *)&hist[(int64_t)(c0 + u) * kSortBuckets + b0] = make_int4(run[0], run[1], run[2], run[3]);
+        run[0] += v[u].x;
+        run[1] += v[u].y;
+        run[2] += v[u].z;
+        run[3] += v[u].w;
+      }
+  }
+}
+
+// grid: one workgroup of 256 per chunk.  The chunk's ids and cursors are
+// staged in LDS by the whole workgroup; then wave 0 takes the ids 64 at a
+// time in CSR order: the lanes that share a bucket find each other through
+// one ballot per bucket bit, take consecutive positions in lane order, and
+// the lowest of them advances the bucket's cursor.
+__global__ __launch_bounds__(256) void sort_scatter_kernel(const int32_t *__restrict__ tok, int n, int64_t vocab,
+                                                          const int32_t *__restrict__ first,
+                                                          int32_t *__restrict__ sorted_tok, int32_t *__restrict__ inv) {
+  __shared__ __attribute__((aligned(16))) int cur[kSortBuckets];
+  __shared__ __attribute__((aligned(16))) int32_t ids[kSortChunk];
+  const int lane = threadIdx.x & 63;
+  const int r0 = blockIdx.x * kSortChunk, r1 = min(n, r0 + kSortChunk);
+  {
+    static_assert(kSortBuckets == 4 * 4 * 256 && kSortChunk == 4 * 4 * 256, "4 x 16 bytes per thread");
+    int4 cv[4], iv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = 4 * (threadIdx.x + 256 * u);
+      cv[u] = *(const int4 *)&first[(int64_t)blockIdx.x * kSortBuckets + i];
+      iv[u] = make_int4(r0 + i < r1 ? tok[r0 + i] : 0, r0 + i + 1 < r1 ? tok[r0 + i + 1] : 0,
+                        r0 + i + 2 < r1 ? tok[r0 + i + 2] : 0, r0 + i + 3 < r1 ? tok[r0 + i + 3] : 0);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = 4 * (threadIdx.x + 256 * u);
+      *(int4 *)&cur[i] = cv[u];
+      *(int4 *)&ids[i] = iv[u];
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x >= 64) return;
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));  // lanes below this one
+  for (int base = r0; base < r1; base += 64) {
+    const int r = base + lane;
+    const bool valid = r < r1;
+    const int32_t t = valid ? ids[r - r0] : 0;
+    const int b = sort_bucket(t, vocab);
+    uint64_t same = __ballot(valid);
+#pragma unroll
+    for (int bit = 0; bit < 12; ++bit) {  // kSortBuckets = 2^12
+      const bool on = (b >> bit) & 1;
+      const uint64_t m = __ballot(on);
+      same &= on ? m : ~m;
+    }
+    const int rank = __popcll(same & lt), cnt = __popcll(same);
+    const int pos = cur[b] + rank;  // every lane reads before the leaders write (in order within the wave)
+    if (valid) {
+      sorted_tok[pos] = t;
+      inv[r] = pos;
+      if (rank == 0) cur[b] = pos + cnt;
+    }
+  }
+}
+
+static size_t sort_ws_bytes(int total_rows) {
+  const size_t nchunks = ((size_t)total_rows + kSortChunk - 1) / kSortChunk;
+  return 2 * align256((size_t)total_rows * 4) + align256(nchunks * kSortBuckets * 4);
+}
+
 SM_API size_t sm_merge_workspace_bytes(int total_rows, int num_spans, int d, sm_dtype dt) {
   if (total_rows < 0 || num_spans < 0 || d <= 0) return 0;
   const size_t es = dt == SM_BF16 ? 2 : 4;
   return align256((size_t)total_rows * d * es) + align256((size_t)num_spans * d * es) +
-         align256((size_t)num_spans * d * 4);
+         align256((size_t)num_spans * d * 4) + sort_ws_bytes(total_rows);
 }
 
 // Argument checks shared by the merge entry points.
@@ -1476,6 +1616,23 @@ SM_API sm_status sm_merge_spans(const void *emb, int64_t emb_rows, const int32_t
   void *g1 = wsb;
   void *cbuf = wsb + align256((size_t)total_rows * d * es);
   float *ybuf = (float *)(wsb + align256((size_t)total_rows * d * es) + align256((size_t)num_spans * d * es));
+  if (dt == SM_BF16 && total_rows > kSkinnyMaxM && use_gemm256(total_rows, d, d)) {
+    // the first stage in token-id order (see sort_count_kernel)
+    char *sw = (char *)ybuf + align256((size_t)num_spans * d * 4);
+    int32_t *sorted_tok = (int32_t *)sw;
+    int32_t *inv = (int32_t *)(sw + align256((size_t)total_rows * 4));
+    int32_t *hist = (int32_t *)(sw + 2 * align256((size_t)total_rows * 4));
+    const int nchunks = (total_rows + kSortChunk - 1) / kSortChunk;
+    hipLaunchKernelGGL(sort_count_kernel, dim3(nchunks), dim3(256), 0, stream, row_idx, total_rows, emb_rows, hist);
+    hipLaunchKernelGGL(sort_scan_kernel, dim3(1), dim3(1024), 0, stream, hist, nchunks);
+    hipLaunchKernelGGL(sort_scatter_kernel, dim3(nchunks), dim3(256), 0, stream, row_idx, total_rows, emb_rows,
+                       (const int32_t *)hist, sorted_tok, inv);
+    if (hipGetLastError() != hipSuccess) return SM_EHIP;
+    const sm_status st = first_stage(emb, sorted_tok, emb_rows, total_rows, p, dt, g1, err, stream);
+    if (st != SM_OK) return st;
+    return pool_and_project(g1, inv, total_rows, total_rows, span_offsets, num_spans, p, dt, cbuf, ybuf, out, err,
+                            stream);
+  }
   const sm_status st = first_stage(emb, row_idx, emb_rows, total_rows, p, dt, g1, err, stream);
   if (st != SM_OK) return st;
   return pool_and_project(g1, nullptr, total_rows, total_rows, span_offsets, num_spans, p, dt, cbuf, ybuf, out, err,

@@ -167,6 +167,43 @@ def test_merge_bad_row_index_sets_einval(orc):
     assert err == sm.ERR_EINVAL
 
 
+def test_merge_sorted_rows_bad_ids_and_repeat(orc):
+    """A bf16 batch large enough for the 256-tile first stage, which runs in
+    token-id order (rows sorted by a counting sort, G1 read back through the
+    inverse permutation): ids outside the table set EINVAL and are read as
+    row 0, every other span is pooled as usual, and a second call gives the
+    same bits (the permutation does not depend on timing)."""
+    d, S, vocab = 512, 17000, 3000
+    rng = np.random.RandomState(91)
+    lens = rng.randint(1, 4, size=S)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    R = int(offs[-1])
+    assert (R + 255) // 256 * (d // 256) >= 256 and R % 4096
+    # a skewed id law: a tenth of the rows share 5 ids, so some buckets are large
+    row_idx = rng.randint(0, vocab, size=R).astype(np.int32)
+    hot = rng.rand(R) < 0.1
+    row_idx[hot] = rng.randint(0, 5, size=int(hot.sum()))
+    bad_spans = [5, S // 2, S - 1]
+    bad_ids = [-7, vocab, vocab + 123]
+    for s, b in zip(bad_spans, bad_ids):
+        row_idx[offs[s]] = b
+    g = wl.generator(d + 7)
+    emb = wl.randn((vocab, d), torch.bfloat16, g, std=0.02)
+    params = wl.make_merge_params(d, 4, torch.bfloat16, g, spread=True)
+    say("merge sorted rows, bad ids and repeat", d, S, "rows", R)
+    out, err = _gpu_merge(emb.to(dev()), row_idx, offs, params, 4, torch.bfloat16)
+    assert err == sm.ERR_EINVAL
+    out2, err2 = _gpu_merge(emb.to(dev()), row_idx, offs, params, 4, torch.bfloat16)
+    assert err2 == sm.ERR_EINVAL and torch.equal(out.view(torch.int16), out2.view(torch.int16))
+    fixed = row_idx.copy()
+    fixed[(fixed < 0) | (fixed >= vocab)] = 0
+    sample = np.unique(np.concatenate([rng.choice(S, 300, replace=False), bad_spans, [0, 1]]))
+    ref = _oracle(orc, wl.to_f64(emb), fixed, offs, params, 4, sample=sample)
+    e = rel_l2_max(out.float().numpy()[sample], ref)
+    say("rel_l2_max", e)
+    assert e <= TOL[torch.bfloat16]
+
+
 @pytest.mark.parametrize("d,S", [(4096, 16), (3584, 128), (8192, 4)])
 def test_merge_decode_time_batches(orc, d, S):
     """Decode-time merges: one freshly completed span of n = 2..4 tokens per
