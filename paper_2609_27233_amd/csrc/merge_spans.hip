@@ -157,11 +157,11 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_nt_gelu(const uint16_t *__re
 // One k-tile is four k steps of 16 MFMAs.  Each wave holds a whole k-tile
 // of fragments in registers (128 VGPRs): during k step 0 it reads those of
 // k steps 1-3, then waits for them and passes a barrier, after which the
-// stage is free; k steps 1 and 2 load the k-tile after next into it (one
-// load every other MFMA, so the CU's requests reach the L2 evenly); before
+// stage is free; k steps 1 to 3 load the k-tile after next into it (one
+// load every third MFMA, so the CU's requests reach the L2 evenly); before
 // k step 3 each wave waits for its own loads of the next k-tile and passes
 // a second barrier, and k step 3 reads the next k-tile's first fragments.
-// Each load thus has five to six k steps to land.  The waits are explicit
+// Each load thus has four to six k steps to land.  The waits are explicit
 // s_waitcnt and the instruction order is pinned by a scheduling barrier
 // after each MFMA.
 //
@@ -308,12 +308,12 @@ __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
   // accumulators, each followed by
   //  * k step 0: two of the 24 fragment reads of k steps 1-3 (after MFMAs
   //    0-11);
-  //  * k steps 1 and 2: every other MFMA, one of the 16 loads of k-tile
-  //    kt + 2 into this (by then free) stage; past the end of K the last
-  //    k-tile is loaded again (never read), so that every wait counts the
-  //    same loads;
-  //  * k step 3: one of the 8 fragment reads of k step 0 of k-tile kt + 1
-  //    (after MFMAs 0-7), from the other stage.
+  //  * k steps 1, 2 and 3: every third MFMA, one of the 16 loads of k-tile
+  //    kt + 2 into this (by then free) stage (6, 5 and 5 of them); past the
+  //    end of K the last k-tile is loaded again (never read), so that every
+  //    wait counts the same loads;
+  //  * k step 3: also one of the 8 fragment reads of k step 0 of k-tile
+  //    kt + 1 (after MFMAs 0-7), from the other stage.
 #define SM_KSTEP(ST, KS)                                                                             \
   {                                                                                                  \
     const int kn2_ = min(kt + 2, nk - 1);                                                            \
@@ -328,19 +328,22 @@ __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
           fb[rk_][rq_] = *(const u32x4_t *)(sb + (ST) * kLStageBytes + b_off + fo[rk_] + rq_ * 4096); \
         }                                                                                            \
       } else if ((KS) == 1 || (KS) == 2) {                                                           \
-        if ((g & 1) == 0) load_q(kn2_, (ST), ((KS) - 1) * 8 + (g >> 1));                             \
-      } else if (g < 8) {                                                                            \
-        const int o_ = ((ST) ^ 1) * kLStageBytes + fo[0] + (g >> 1) * 4096;                          \
-        if (g & 1) fb[0][g >> 1] = *(const u32x4_t *)(sb + b_off + o_);                              \
-        else fa[0][g >> 1] = *(const u32x4_t *)(sa + a_off + o_);                                    \
+        if (g % 3 == 0 && ((KS) == 1 || g < 15)) load_q(kn2_, (ST), ((KS) - 1) * 6 + g / 3);         \
+      } else {                                                                                       \
+        if (g < 8) {                                                                                 \
+          const int o_ = ((ST) ^ 1) * kLStageBytes + fo[0] + (g >> 1) * 4096;                        \
+          if (g & 1) fb[0][g >> 1] = *(const u32x4_t *)(sb + b_off + o_);                            \
+          else fa[0][g >> 1] = *(const u32x4_t *)(sa + a_off + o_);                                  \
+        }                                                                                            \
+        if (g % 3 == 1 && g < 15) load_q(kn2_, (ST), 11 + g / 3);                                    \
       }                                                                                              \
       __builtin_amdgcn_sched_barrier(0);                                                             \
     }                                                                                                \
   }
   // A k-tile: k step 0; this wave's fragment reads done, barrier (the stage
   // is free: every wave holds the k-tile in registers); k steps 1 and 2;
-  // this wave's loads of k-tile kt + 1 done (those of kt + 2 may still be
-  // in flight), barrier (k-tile kt + 1 is in LDS); k step 3.
+  // this wave's loads of k-tile kt + 1 done (the 11 of kt + 2 issued since
+  // may still be in flight), barrier (k-tile kt + 1 is in LDS); k step 3.
 #define SM_KTILE(ST)                                                                                 \
   {                                                                                                  \
     SM_KSTEP(ST, 0);                                                                                 \
@@ -349,7 +352,7 @@ __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
     __builtin_amdgcn_sched_barrier(0);                                                               \
     SM_KSTEP(ST, 1);                                                                                 \
     SM_KSTEP(ST, 2);                                                                                 \
-    wait_vmcnt_lgkm0<16>();                                                                          \
+    wait_vmcnt_lgkm0<11>();                                                                          \
     __builtin_amdgcn_s_barrier();                                                                    \
     __builtin_amdgcn_sched_barrier(0);                                                               \
     SM_KSTEP(ST, 3);                                                                                 \
