@@ -161,15 +161,19 @@ __device__ __forceinline__ int block_inclusive_scan(int v, int *red, int *total)
   return v + before;
 }
 
-// GELU(x) = x Phi(x) with Phi(x) = erfc(-x / sqrt 2) / 2.  erfc(z) for
-// z >= 0 comes from the Chebyshev-fitted formula of Numerical Recipes (2nd
-// ed., section 6.2, function erfcc: t = 1 / (1 + z / 2), erfc = t exp(-z^2 +
+// GELU(x) = x Phi(x) with Phi(x) = erfc(-x / sqrt 2) / 2, written as
+// max(x, 0) - |x| erfc(z) / 2 with z = |x| / sqrt 2 (for x >= 0,
+// x Phi(x) = x - x erfc(z) / 2; for x < 0 it is x erfc(z) / 2).  erfc(z)
+// comes from the Chebyshev-fitted formula of Numerical Recipes (2nd ed.,
+// section 6.2, function erfcc: t = 1 / (1 + z / 2), erfc = t exp(-z^2 +
 // P(t)) with a degree-9 polynomial P, fractional error below 1.2e-7 for
-// every z).  One reciprocal, one exponential and ten fused multiply-adds;
-// the form 0.5 x (1 + erf(x / sqrt 2)) costs about three times as many
-// instructions and loses all relative accuracy for x below about -4, where
-// 1 + erf cancels.  Measured against erfc in double: relative error below
-// 1.3e-6 for |x| <= 3, absolute error below 4e-7 everywhere.
+// every z); the factor 1 / 2 and the 1 / sqrt 2 of |x| = sqrt 2 z go into
+// the exponent as -1/2 (log2 of sqrt 2 / 2).  One reciprocal, one
+// exponential and twelve fused multiply-adds or multiplies; the form
+// 0.5 x (1 + erf(x / sqrt 2)) costs about twice the instructions and loses
+// all relative accuracy for x below about -4, where 1 + erf cancels.
+// Measured against erfc in double: relative error below 1.3e-6 for
+// |x| <= 3, absolute error below 4e-7 everywhere.
 __device__ __forceinline__ float gelu_erf(float x) {
   const float z = fabsf(x) * 0.70710678118654752f;
   const float t = __builtin_amdgcn_rcpf(fmaf(0.5f, z, 1.0f));
@@ -182,8 +186,9 @@ __device__ __forceinline__ float gelu_erf(float x) {
   p = fmaf(t, p, 0.37409196f);
   p = fmaf(t, p, 1.00002368f);
   p = fmaf(t, p, -1.26551223f);
-  const float e = 0.5f * t * __builtin_amdgcn_exp2f(fmaf(-z, z, p) * 1.4426950408889634f);  // erfc(z) / 2
-  return x * (x >= 0.f ? 1.f - e : e);
+  // t 2^((P - z^2) log2 e - 1/2) = erfc(z) / (2 sqrt 2) = (erfc(z) / 2) / (|x| / z)
+  const float te = t * __builtin_amdgcn_exp2f(fmaf(fmaf(-z, z, p), 1.4426950408889634f, -0.5f));
+  return fmaf(-z, te, fmaxf(x, 0.f));
 }
 
 __device__ __forceinline__ void set_err(int32_t *err, int bit) {
