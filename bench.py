@@ -50,8 +50,8 @@ METRIC = "decode-attention tokens/s + achieved HBM GB/s over span-compacted KV c
 # WRITE_SIZE runs (see profiles/decode_step_llama3-8b-layer.md): scaled
 # measured bytes per launch divided by the algorithmic bytes of the same
 # launches.  Valid only for the kernel source it was measured on.
-TRAFFIC_RATIO = 1.0153
-TRAFFIC_SOURCE_SHA256 = {"decode_attn.hip": "7ebac19459e1d185ca656f1d77649011df215d63ea84b769a15ccf7f6932dd37", "common.hpp": "b33d848d212d0d3e660d0e361606225f38e6024217e8cff49c2cdf89b79a2751"}
+TRAFFIC_RATIO = 1.0156
+TRAFFIC_SOURCE_SHA256 = {"decode_attn.hip": "7ebac19459e1d185ca656f1d77649011df215d63ea84b769a15ccf7f6932dd37", "common.hpp": "3a781c03722dbc429c51a46492495ab49231891a56fcc322a70bd2033200c04d"}
 
 
 def log(*a):
