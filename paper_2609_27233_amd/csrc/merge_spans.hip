@@ -1076,7 +1076,10 @@ __global__ __launch_bounds__(256, CPL <= 2 ? 3 : 2) void pool_slices_kernel(cons
         }
       }
   }
-  const float inv_sqrt_dh = 1.0f / sqrtf((float)dh), n_slice = (float)slice;
+  // scores in base 2 (log2 e folded into 1 / sqrt(dh)): exp2 is one instruction; the
+  // softmax is the same.  Divisions by the slice width and d become products.
+  const float l2_sqrt_dh = 1.4426950408889634f / sqrtf((float)dh), n_slice = (float)slice;
+  const float inv_ns = 1.0f / n_slice, inv_d = 1.0f / (float)d;
 
   // the next span's row range is requested a span ahead
   int nx0 = 0, nx1 = 0;
@@ -1177,36 +1180,36 @@ __global__ __launch_bounds__(256, CPL <= 2 ? 3 : 2) void pool_slices_kernel(cons
 #pragma unroll
             for (int ww = 0; ww < 4; ++ww) {
               const float a1 = sh_s1[rr][ww];
-              mw[ww] = sh_k[rr][ww] + a1 / n_slice;
+              mw[ww] = sh_k[rr][ww] + a1 * inv_ns;
               mean += mw[ww];
-              m2 += sh_s2[rr][ww] - a1 * (a1 / n_slice);
+              m2 += sh_s2[rr][ww] - a1 * (a1 * inv_ns);
             }
             mean *= 0.25f;
 #pragma unroll
             for (int ww = 0; ww < 4; ++ww) m2 += n_slice * (mw[ww] - mean) * (mw[ww] - mean);
-            iv[rr] = 1.0f / sqrtf(fmaxf(m2, 0.f) / d + eps);
+            iv[rr] = __builtin_amdgcn_rsqf(fmaxf(m2, 0.f) * inv_d + eps);
             float t = 0.f, dq = 0.f;
             for (int ww = wf; ww <= wl; ++ww) {
               const int hs = hh - (ww * slice) / dh;
               t += sh_t[rr][ww][hs] + (sh_k[rr][ww] - mean) * sh_c[ww][hs];
               dq += sh_dq[ww][hs];
             }
-            sc[rr] = (iv[rr] * t + dq) * inv_sqrt_dh;
+            sc[rr] = (iv[rr] * t + dq) * l2_sqrt_dh;
             gmax = fmaxf(gmax, sc[rr]);
             if (hh == 0) sh_mu[rr] = mean;
           }
-        const float Mn = fmaxf(M, gmax), scale = expf(M - Mn);  // 0 for the first group
+        const float Mn = fmaxf(M, gmax), scale = __builtin_amdgcn_exp2f(M - Mn);  // 0 for the first group
         Z *= scale;
 #pragma unroll
         for (int rr = 0; rr < R; ++rr)
           if (rr < nr) {
-            const float p = expf(sc[rr] - Mn);
+            const float p = __builtin_amdgcn_exp2f(sc[rr] - Mn);
             Z += p;
             sh_a[rr][hh] = p * iv[rr];
           }
         M = Mn;
         sh_scale[hh] = scale;
-        if (g0 + R >= n) sh_iz[hh] = 1.0f / Z;
+        if (g0 + R >= n) sh_iz[hh] = __builtin_amdgcn_rcpf(Z);
       }
       lds_barrier();
       // fold the group into this wave's weighted sum (the rows are unpacked
