@@ -1080,6 +1080,22 @@ __global__ __launch_bounds__(256, CPL <= 2 ? 3 : 2) void pool_slices_kernel(cons
   // softmax is the same.  Divisions by the slice width and d become products.
   const float l2_sqrt_dh = 1.4426950408889634f / sqrtf((float)dh), n_slice = (float)slice;
   const float inv_ns = 1.0f / n_slice, inv_d = 1.0f / (float)d;
+  // thread hh < h: the slices head hh meets, its index within each, and
+  // its constants C_wh (per slice) and D_h (all slices)
+  float hc[4] = {0.f, 0.f, 0.f, 0.f}, hdq = 0.f;
+  int hsl[4] = {0, 0, 0, 0}, hwf = 0, hwl = -1;
+  __syncthreads();  // sh_c, sh_dq
+  if (tid < h) {
+    hwf = (tid * dh) / slice;
+    hwl = (tid * dh + dh - 1) / slice;
+#pragma unroll
+    for (int ww = 0; ww < 4; ++ww)
+      if (ww >= hwf && ww <= hwl) {
+        hsl[ww] = tid - (ww * slice) / dh;
+        hc[ww] = sh_c[ww][hsl[ww]];
+        hdq += sh_dq[ww][hsl[ww]];
+      }
+  }
 
   // the next span's row range is requested a span ahead
   int nx0 = 0, nx1 = 0;
@@ -1171,7 +1187,7 @@ __global__ __launch_bounds__(256, CPL <= 2 ? 3 : 2) void pool_slices_kernel(cons
       // the group's row statistics and scores, folded into the running
       // softmax: thread hh < h takes head hh
       if (tid < h) {
-        const int hh = tid, wf = (hh * dh) / slice, wl = (hh * dh + dh - 1) / slice;
+        const int hh = tid;
         float sc[R], iv[R], gmax = -INFINITY;
 #pragma unroll
         for (int rr = 0; rr < R; ++rr)
@@ -1188,13 +1204,11 @@ __global__ __launch_bounds__(256, CPL <= 2 ? 3 : 2) void pool_slices_kernel(cons
 #pragma unroll
             for (int ww = 0; ww < 4; ++ww) m2 += n_slice * (mw[ww] - mean) * (mw[ww] - mean);
             iv[rr] = __builtin_amdgcn_rsqf(fmaxf(m2, 0.f) * inv_d + eps);
-            float t = 0.f, dq = 0.f;
-            for (int ww = wf; ww <= wl; ++ww) {
-              const int hs = hh - (ww * slice) / dh;
-              t += sh_t[rr][ww][hs] + (sh_k[rr][ww] - mean) * sh_c[ww][hs];
-              dq += sh_dq[ww][hs];
-            }
-            sc[rr] = (iv[rr] * t + dq) * l2_sqrt_dh;
+            float t = 0.f;
+#pragma unroll
+            for (int ww = 0; ww < 4; ++ww)
+              if (ww >= hwf && ww <= hwl) t += sh_t[rr][ww][hsl[ww]] + (sh_k[rr][ww] - mean) * hc[ww];
+            sc[rr] = (iv[rr] * t + hdq) * l2_sqrt_dh;
             gmax = fmaxf(gmax, sc[rr]);
             if (hh == 0) sh_mu[rr] = mean;
           }
