@@ -1327,21 +1327,29 @@ static hipError_t launch_pool(const T *G1, const int32_t *gidx, int64_t g_rows, 
 
 // LN_o over fp32 rows Y -> out (storage dtype), one workgroup per row; the
 // row, the gain and the bias are all requested before the first reduction.
-template <typename T>
-__global__ __launch_bounds__(kPoolThreads) void ln_rows_kernel(const float *__restrict__ Y,
+template <typename T, typename YT = float>
+__global__ __launch_bounds__(kPoolThreads) void ln_rows_kernel(const YT *__restrict__ Y,
                                                                const T *__restrict__ g, const T *__restrict__ b,
                                                                float eps, int d, T *__restrict__ out) {
   constexpr int kMaxV = kMaxD / 4 / kPoolThreads;
   __shared__ float red[kPoolThreads / 64];
   const int s = blockIdx.x, tid = threadIdx.x;
   const int nvec = d / 4;
-  const float *row = Y + (int64_t)s * d;
+  const YT *row = Y + (int64_t)s * d;
   float x[kMaxV][4], gv[kMaxV][4], bv[kMaxV][4];
 #pragma unroll
   for (int u = 0; u < kMaxV; ++u) {
     const int v = tid + u * kPoolThreads;
     if (v < nvec) {
-      load_vec<float>(row + v * 4, x[u]);
+      if constexpr (sizeof(YT) == 2) {
+        const uint2 yy = *(const uint2 *)(row + v * 4);
+        x[u][0] = __uint_as_float(yy.x << 16);
+        x[u][1] = __uint_as_float(yy.x & 0xffff0000u);
+        x[u][2] = __uint_as_float(yy.y << 16);
+        x[u][3] = __uint_as_float(yy.y & 0xffff0000u);
+      } else {
+        load_vec<float>((const float *)row + v * 4, x[u]);
+      }
       if constexpr (sizeof(T) == 2) {
         const uint2 gg = *(const uint2 *)(g + v * 4), bb = *(const uint2 *)(b + v * 4);
         gv[u][0] = __uint_as_float(gg.x << 16);
@@ -1591,10 +1599,14 @@ static sm_status pool_and_project(const void *G1, const int32_t *gidx, int64_t g
       launch_skinny<float>((const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
                            (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, ybuf, num_spans, d, d, err, stream);
     else if (use_gemm256(num_spans, d, d)) {
-      if (launch_gemm256<float>((const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
-                                (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, ybuf, num_spans, d, d, err,
-                                stream) != hipSuccess)
+      if (launch_gemm256<uint16_t>((const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
+                                   (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, (uint16_t *)ybuf, num_spans, d,
+                                   d, err, stream) != hipSuccess)
         return SM_EHIP;
+      hipLaunchKernelGGL((ln_rows_kernel<uint16_t, uint16_t>), dim3(num_spans), dim3(kPoolThreads), 0, stream,
+                         (const uint16_t *)ybuf, (const uint16_t *)p->g_o, (const uint16_t *)p->beta_o, p->ln_eps, d,
+                         (uint16_t *)out);
+      return hipGetLastError() == hipSuccess ? SM_OK : SM_EHIP;
     } else
       hipLaunchKernelGGL(gemm_bf16_nt_gelu<float>, dim3(d / kBN, (num_spans + kBM - 1) / kBM), dim3(256), 0,
                          stream, (const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
