@@ -160,7 +160,11 @@ size_t sm_merge_workspace_bytes(int total_rows, int num_spans, int d,
  *   a_i = softmax_j(P[j, head i] . q_i / sqrt(d_h)),  o_i = sum_j a_i[j] P[j, head i]
  *   z_s = LN_o(GELU(Linear_o([o_1; ...; o_h])))
  *
- * GELU is the exact erf form; LayerNorm uses the biased variance.
+ * GELU is the exact erf form (evaluated through erfc to about 1e-6
+ * relative); LayerNorm uses the biased variance.  bf16 calls round the
+ * intermediate rows to bf16 and accumulate in fp32; large bf16 calls run
+ * the first projection with the rows in token-id order, so the rounding of
+ * one span's result can depend on the other spans of the call.
  *
  *  emb           [emb_rows][d] static embedding table (dtype dt)
  *  row_idx       [total_rows] row of emb for each span token, spans stored
