@@ -1274,7 +1274,7 @@ def main():
                     help="streams the resident batches' decode steps are spread over (batch r on stream r %% lanes)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: this build measures the single-GPU hot path "
+        print(f"bench.py runs on one GPU only: it measures the hot path on a single GPU "
               f"(--gpus {args.gpus} is not supported)", file=sys.stderr)
         sys.exit(2)
 
