@@ -437,11 +437,12 @@ __global__ __launch_bounds__(kLThreads, 1) void gemm256_bf16_nt_gelu(
 }
 
 // Output tiles from which the 256-tile GEMM stages a bf16 epilogue through
-// LDS (several waves of tiles, so that other workgroups' main loops overlap
-// it).  Measured: GEMM1 of the 70B-shaped batch (17,984 tiles) 19.6 -> 18.1
-// ms; at 1,856 tiles equal or faster; at 256 to 624 tiles, and for the fp32
-// output of the second projection at any size, slower or equal.
-constexpr int kStagedMinTiles = 1024;
+// LDS.  Measured on the four-wave kernel: GEMM1 of the 70B-shaped batch
+// (17,984 tiles) much faster staged (the direct stores wrote 4x the bytes);
+// the second projection of the 16 x 4096 prompt batch (624 tiles) about 1%
+// faster; so every bf16 output is staged (256 tiles is the kernel's
+// minimum).  fp32 output stays direct (two LDS passes measured no better).
+constexpr int kStagedMinTiles = 256;
 
 static bool use_gemm256(int M, int N, int K) {
   return N % kLN == 0 && K % (2 * kLK) == 0 && K >= 2 * kLK * kLStages &&
