@@ -1396,6 +1396,83 @@ __global__ __launch_bounds__(kPoolThreads) void ln_rows_kernel(const YT *__restr
   }
 }
 
+// LN_o over bf16 rows of d = NV * 2048 (256 threads x NV 16-byte groups),
+// for large batches: persistent workgroups take rows blockIdx.x,
+// blockIdx.x + gridDim.x, ...; each loads the gain and bias once (one
+// workgroup per row re-read them from L2 for every row, as many bytes as
+// the row itself) and issues the next row's loads before this row's two
+// reductions.  The arithmetic is that of ln_rows_kernel: mean, then the
+// mean of squared deviations, in fp32; bf16 out, rounded to nearest even.
+template <int NV>
+__global__ __launch_bounds__(kPoolThreads) void ln_rows_bf16_kernel(const uint16_t *__restrict__ Y,
+                                                                    const uint16_t *__restrict__ g,
+                                                                    const uint16_t *__restrict__ b, float eps,
+                                                                    int d, int rows, uint16_t *__restrict__ out) {
+  __shared__ float red[kPoolThreads / 64];
+  const int tid = threadIdx.x;
+  u32x4_t gq[NV], bq[NV], xq[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int col = (tid + v * kPoolThreads) * 8;
+    gq[v] = *(const u32x4_t *)(g + col);
+    bq[v] = *(const u32x4_t *)(b + col);
+    xq[v] = *(const u32x4_t *)(Y + (int64_t)blockIdx.x * d + col);
+  }
+  for (int s = blockIdx.x; s < rows; s += gridDim.x) {
+    const int sn = min(s + (int)gridDim.x, rows - 1);  // (the last row's loads are repeated, never used)
+    u32x4_t nq[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) nq[v] = *(const u32x4_t *)(Y + (int64_t)sn * d + (tid + v * kPoolThreads) * 8);
+    float x[NV][8];
+    float sum = 0.f;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      unpack_vec<uint16_t>(xq[v], x[v]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sum += x[v][e];
+    }
+    const float mean = block_sum(sum, red) / d;
+    float sq = 0.f;
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sq += (x[v][e] - mean) * (x[v][e] - mean);
+    const float inv = 1.0f / sqrtf(block_sum(sq, red) / d + eps);
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      float gf[8], bf[8], y[8];
+      unpack_vec<uint16_t>(gq[v], gf);
+      unpack_vec<uint16_t>(bq[v], bf);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = gf[e] * (x[v][e] - mean) * inv + bf[e];
+      store_vec<uint16_t>(out + (int64_t)s * d + (tid + v * kPoolThreads) * 8, y);
+      xq[v] = nq[v];
+    }
+  }
+}
+
+// LN_o of bf16 rows: the persistent form where d allows it (rows > 0)
+static hipError_t launch_ln_bf16(const uint16_t *Y, const uint16_t *g, const uint16_t *b, float eps, int d,
+                                 int rows, uint16_t *out, hipStream_t stream) {
+  const int nv = d % (8 * kPoolThreads) == 0 ? d / (8 * kPoolThreads) : 0;
+#define SM_LN_CASE(NV)                                                                                   \
+  case NV: {                                                                                             \
+    const int nb = resident_blocks(ln_rows_bf16_kernel<NV>, kPoolThreads);                               \
+    hipLaunchKernelGGL(ln_rows_bf16_kernel<NV>, dim3(rows < nb ? rows : nb), dim3(kPoolThreads), 0, stream, Y, g, \
+                       b, eps, d, rows, out);                                                            \
+    return hipGetLastError();                                                                            \
+  }
+  switch (nv) {
+    SM_LN_CASE(1) SM_LN_CASE(2) SM_LN_CASE(3) SM_LN_CASE(4)
+    default:
+      break;
+  }
+#undef SM_LN_CASE
+  hipLaunchKernelGGL((ln_rows_kernel<uint16_t, uint16_t>), dim3(rows), dim3(kPoolThreads), 0, stream, Y, g, b, eps,
+                     d, out);
+  return hipGetLastError();
+}
+
 }  // namespace sm
 
 using namespace sm;
@@ -1604,10 +1681,10 @@ static sm_status pool_and_project(const void *G1, const int32_t *gidx, int64_t g
                                    (const uint16_t *)p->W_o, (const uint16_t *)p->b_o, (uint16_t *)ybuf, num_spans, d,
                                    d, err, stream) != hipSuccess)
         return SM_EHIP;
-      hipLaunchKernelGGL((ln_rows_kernel<uint16_t, uint16_t>), dim3(num_spans), dim3(kPoolThreads), 0, stream,
-                         (const uint16_t *)ybuf, (const uint16_t *)p->g_o, (const uint16_t *)p->beta_o, p->ln_eps, d,
-                         (uint16_t *)out);
-      return hipGetLastError() == hipSuccess ? SM_OK : SM_EHIP;
+      return launch_ln_bf16((const uint16_t *)ybuf, (const uint16_t *)p->g_o, (const uint16_t *)p->beta_o,
+                            p->ln_eps, d, num_spans, (uint16_t *)out, stream) == hipSuccess
+                 ? SM_OK
+                 : SM_EHIP;
     } else
       hipLaunchKernelGGL(gemm_bf16_nt_gelu<float>, dim3(d / kBN, (num_spans + kBM - 1) / kBM), dim3(256), 0,
                          stream, (const uint16_t *)cbuf, (const int32_t *)nullptr, (int64_t)num_spans,
